@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Throughput of the AFNO spectral filter on one MI355X, as one JSON line.
+
+A step is one full filter call (W-axis forward transform, column kernel with the
+H transforms and the block MLP, W-axis inverse transform + residual) on the
+90 x 180 x 768 bf16 workload with B = 4 (8 blocks of 96; synthetic N(0,1) fields
+scaled per channel by U(0.5, 2), complex weights N(0, 0.02^2), lambda 0.01, keep 1),
+with inputs resident in HBM.  value = samples per second = B / (time per step).
+
+Alongside: per-kernel HIP-event times on the launch stream over the same timed region,
+the roofline of the dominant kernel (algorithmic bytes or FLOPs per launch divided by
+its mean launch time), measured HBM traffic from stored rocprofv3 counters when they
+belong to the current kernel sources, the 100-member ensemble workload, and the float64
+CPU oracle timed on a bounded sample on the host cores.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-ensemble] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3       # fp32 matrix
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_afno90x180_c768_nb8_bf16_b4.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2208_05419_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def algorithmic_work(wl, es: int):
+    """Per-launch algorithmic bytes and FLOPs of each kernel (minimum traffic of each
+    standalone pass: read its input once, write its output once)."""
+    B, H, W, C, bs = wl.B, wl.H, wl.W, wl.C, wl.bs
+    kept_h = int((H // 2 + 1) * wl.keep)
+    kw = int((W // 2 + 1) * wl.keep)
+    rows_kept = sum(1 for r in range(H) if abs(r if r <= H // 2 else r - H) < kept_h)
+    x_bytes = B * H * W * C * es
+    s_bytes = B * H * kw * C * 2 * es           # spectrum workspace, complex in dtype
+    flops = 16 * C * bs * B * rows_kept * kw     # two complex GEMMs, 8 real FLOP per complex MAC
+    return {
+        "row_r2c": {"bytes": x_bytes + s_bytes, "flops": 0},
+        "column": {"bytes": 2 * s_bytes, "flops": flops},
+        "row_c2r": {"bytes": s_bytes + 2 * x_bytes, "flops": 0},
+    }
+
+
+def time_workload(wl, steps: int, warmup: int, seed: int = 0):
+    import numpy as np
+    import torch
+
+    import paper_2208_05419_amd as afno
+    from paper_2208_05419_amd import synth
+
+    def dev(a):
+        if wl.dtype == "fp32":
+            return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    x = dev(synth.make_x(wl, seed=seed))
+    w = {k: dev(v) for k, v in synth.make_weights(wl, seed=seed).items()}
+    out = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep,
+                            out=out, stream=stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    afno.profile_begin(steps)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    kernel_ms, calls = afno.profile_end()
+    total_ms = t_start.elapsed_time(t_end)
+    del x, w, out
+    torch.cuda.empty_cache()
+    return total_ms / steps, {k: v / max(calls, 1) for k, v in kernel_ms.items()}, calls
+
+
+def roofline(wl, kern_ms: dict, es: int):
+    work = algorithmic_work(wl, es)
+    per = {}
+    for k, ms in kern_ms.items():
+        s = ms * 1e-3
+        gbs = work[k]["bytes"] / s / 1e9 if s > 0 else 0.0
+        tfl = work[k]["flops"] / s / 1e12 if s > 0 else 0.0
+        per[k] = {"ms": round(ms, 5), "bytes": work[k]["bytes"], "flops": work[k]["flops"],
+                  "GB_s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+        if work[k]["flops"]:
+            peak = BF16_PEAK_TFLOPS if es == 2 else FP32_PEAK_TFLOPS
+            per[k]["TFLOP_s"] = round(tfl, 2)
+            per[k]["mfma_frac"] = round(tfl / peak, 4)
+    dom = max(kern_ms, key=lambda k: kern_ms[k])
+    d = per[dom]
+    peak_tf = BF16_PEAK_TFLOPS if es == 2 else FP32_PEAK_TFLOPS
+    # roofline bound of the dominant kernel: the larger of its two lower-bound times
+    t_hbm = work[dom]["bytes"] / (HBM_PEAK_GBS * 1e9)
+    t_mma = work[dom]["flops"] / (peak_tf * 1e12)
+    if t_mma > t_hbm:
+        roof = {"bound": "mfma", "achieved": d["TFLOP_s"], "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": d["mfma_frac"]}
+    else:
+        roof = {"bound": "hbm", "achieved": d["GB_s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": d["hbm_frac"]}
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_sha256") == kernel_source_hash() and dom in tr.get("kernels", {}):
+            roof["traffic"] = tr["kernels"][dom]["hbm_bytes_per_launch"]
+    except (OSError, ValueError, KeyError):
+        pass
+    return roof, per
+
+
+def cpu_baseline(wl, n_samples: int):
+    import numpy as np
+
+    import oracle
+    from paper_2208_05419_amd import synth
+
+    x = synth.widen(synth.make_x(wl, members=list(range(n_samples))), wl.dtype)
+    w = {k: synth.widen(v, wl.dtype) for k, v in synth.make_weights(wl).items()}
+    t0 = time.perf_counter()
+    oracle.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep)
+    dt = time.perf_counter() - t0
+    del np
+    return {"value": round(n_samples / dt, 4), "unit": "samples/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{n_samples} of the {wl.B} samples of {wl.name} (float64 direct DFT, "
+                      f"{dt:.1f} s wall)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-ensemble", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=2)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this filter runs on one GPU; --gpus must be 1 (no multi-GPU path)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2208_05419_amd as afno
+    from paper_2208_05419_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    afno.load_library()
+    wl = synth.WORKLOADS[synth.HEADLINE]
+    es = 2 if wl.dtype == "bf16" else 4
+    ms, kern_ms, calls = time_workload(wl, args.steps, args.warmup)
+    roof, per_kernel = roofline(wl, kern_ms, es)
+    value = wl.B / (ms * 1e-3)
+    line = {
+        "metric": "AFNO-filter samples/s @90x180x768 bf16",
+        "value": round(value, 2),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C,
+                   "num_blocks": wl.num_blocks, "lambda": wl.lam, "keep_fraction": wl.keep},
+        "roofline": roof,
+        "kernels": per_kernel,
+        "timed_calls": calls,
+    }
+    if not args.no_ensemble:
+        ens = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
+        e_ms, e_kern, _ = time_workload(ens, max(args.steps // 5, 5), max(args.warmup // 5, 3))
+        e_roof, e_per = roofline(ens, e_kern, 2)
+        e_roof["traffic"] = None
+        line["ensemble"] = {"workload": ens.name, "samples_per_s": round(ens.B / (e_ms * 1e-3), 2),
+                            "ms_per_step": round(e_ms, 4), "kernels": e_per, "roofline": e_roof}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_samples)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,131 @@
+/*
+ * afno.h -- C ABI of the MI355X (gfx950) AFNO spectral token-mixing filter.
+ *
+ * The filter is the spatial-mixing step of the FourCastNet AFNO transformer
+ * (section "Model Innovations", the three steps: a 2-D FFT of the token grid, a
+ * block-diagonal MLP applied to every token in Fourier space with weights shared by
+ * all tokens, an inverse FFT), implemented with real-to-complex / complex-to-real
+ * transforms batched over batch and channels, complex weights stored as real arrays
+ * with (re, im) as the fastest index and activations acting on the real and
+ * imaginary parts independently (section "Implementation Details" (b), "Spectral
+ * convolution").  Softshrink, the hard mode cutoff and the residual come from the
+ * AFNO layer the paper builds on.  Every step runs in hand-written HIP kernels.
+ *
+ * For one sample, with Wm = W/2 + 1, nb blocks of bs = C/nb channels, hs = bs:
+ *   X[kh][kw][c] = (1/sqrt(HW)) sum_{h,w} x[h][w][c] exp(-2 pi i (kh h/H + kw w/W)),  kw <= W/2
+ *   for every mode kept by the cutoff and every block k (true complex products):
+ *     v[j] = b1[k][j] + sum_i X[k bs + i] w1[k][i][j];  h[j] = ReLU(Re v[j]) + i ReLU(Im v[j])
+ *     o[i] = b2[k][i] + sum_j h[j] w2[k][j][i]
+ *     Y[k bs + i] = S(Re o[i]) + i S(Im o[i]),  S(v) = v - lambda (v > lambda),
+ *                                              v + lambda (v < -lambda), 0 otherwise
+ *   modes outside the cutoff: Y = 0
+ *   y[h][w][c] = (1/sqrt(HW)) sum_{kh, kw<=W/2} c_kw Re(Y[kh][kw][c] exp(+2 pi i (kh h/H + kw w/W))),
+ *                c_kw = 1 for kw = 0 and kw = W/2, 2 otherwise
+ *   out = x + y, rounded once to the storage dtype.
+ * Hard mode cutoff (keep_fraction f): kept_h = floor((H/2+1) f) and
+ * kept_w = floor((W/2+1) f), both evaluated in double; a mode (kh, kw) is kept when
+ * |kh'| < kept_h, kh' = kh for kh <= H/2 and kh - H above, and kw < kept_w.
+ * f = 1 keeps every mode; when either count is 0 nothing is kept and out = x.
+ */
+#ifndef AFNO_H_
+#define AFNO_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage dtype of x, the weights, the biases and out. */
+typedef enum { AFNO_DTYPE_FP32 = 0, AFNO_DTYPE_BF16 = 1 } afno_dtype_t;
+
+/* Return codes. */
+enum {
+  AFNO_OK = 0,
+  AFNO_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, C % nb != 0, bad lambda/keep/dtype */
+  AFNO_ERR_UNSUPPORTED = -2, /* valid filter this library does not run: see afno_filter_forward */
+  AFNO_ERR_ALIAS = -3,       /* out overlaps an input */
+  AFNO_ERR_HIP = -4          /* a HIP allocation or launch failed; see afno_last_error() */
+};
+
+/*
+ * afno_filter_forward -- out = x + filter(x) (the filter defined above).
+ *
+ *   x    [B][H][W][C]        dtype, row-major (channels fastest), device memory
+ *   w1   [nb][bs][hs][2]     dtype, complex (re, im) fastest, input-major: x @ w1
+ *   b1   [nb][hs][2]         dtype
+ *   w2   [nb][hs][bs][2]     dtype
+ *   b2   [nb][bs][2]         dtype
+ *   B >= 0; H, W, C, num_blocks > 0; C % num_blocks == 0; hs = bs = C / num_blocks
+ *   lambda         softshrink threshold, finite and >= 0
+ *   keep_fraction  hard mode cutoff f, 0 < f <= 1
+ *   dtype          an afno_dtype_t
+ *   out  [B][H][W][C]        dtype, device memory, must not overlap any input
+ *   stream         HIP stream the work is enqueued on (0 = the null stream)
+ *
+ * Ownership: the caller owns every array; all are contiguous device memory on the
+ * current device and must stay valid until the stream has finished the work.  The
+ * library allocates a spectrum workspace of B*H*kept_w*C complex values (8 bytes each
+ * for fp32, 4 for bf16) stream-ordered on `stream` and frees it stream-ordered.
+ * The call is asynchronous: it enqueues on `stream` and returns.
+ * B == 0 returns AFNO_OK without touching the GPU (x and out may then be NULL).
+ * Errors: arguments are validated before any HIP call; on a non-OK return nothing
+ * has been enqueued, except for AFNO_ERR_HIP from a launch, after which out is
+ * undefined.  AFNO_ERR_UNSUPPORTED: H or W not of the form 2^a 3^b 5^c, W odd,
+ * bs not a multiple of 16 or above 128, or a grid too large for on-chip storage
+ * (a column of H complex values x bs channels must fit the 160 KiB LDS of one CU,
+ * H <= 192 for bs = 128, and W <= 1024).
+ * Thread safety: calls from several host threads are safe; calls whose streams
+ * overlap in time only share read-only inputs.
+ */
+int afno_filter_forward(const void* x, const void* w1, const void* b1, const void* w2,
+                        const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                        int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                        void* out, hipStream_t stream);
+
+/*
+ * afno_filter_stage -- diagnostic entry point: runs the filter's kernels up to a stage
+ * and writes that stage's result in float32, for per-stage parity checks.
+ *   stage AFNO_STAGE_SPECTRUM  dst [B][H][Wm][C][2] float32: the forward spectrum X
+ *                              (both axes, ortho-normalised); columns kw >= kept_w
+ *                              are not computed and are written as 0.
+ *   stage AFNO_STAGE_MIXED     dst [B][H][Wm][C][2] float32: Y after the block MLP,
+ *                              softshrink and the cutoff.
+ *   stage AFNO_STAGE_DELTA     dst [B][H][W][C] float32: y = filter(x) before the
+ *                              residual add and before rounding to dtype.
+ * Other arguments, ownership and errors as afno_filter_forward, with dst in place of
+ * out.  The values are what the kernels hold at that point (for bf16 storage the
+ * spectra are bf16-rounded).
+ */
+enum { AFNO_STAGE_SPECTRUM = 1, AFNO_STAGE_MIXED = 2, AFNO_STAGE_DELTA = 3 };
+int afno_filter_stage(const void* x, const void* w1, const void* b1, const void* w2,
+                      const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                      int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                      int stage, float* dst, hipStream_t stream);
+
+/*
+ * Diagnostic per-kernel timing.  afno_profile_begin(max_calls) creates HIP events for
+ * up to max_calls filter calls (process-wide); each later afno_filter_forward call
+ * records an event before its first kernel and after each kernel, on the call's
+ * stream.  afno_profile_end waits for those events, writes the summed milliseconds of
+ * each kernel to kernel_ms[0..2] (0: W-axis forward transform, 1: column kernel
+ * H-transforms + block MLP, 2: W-axis inverse transform + residual) and the number of
+ * timed calls to *calls, and frees the events.  Calls beyond max_calls are not timed.
+ * Returns AFNO_OK, AFNO_ERR_INVALID_ARG (max_calls <= 0, null output, or end without
+ * begin) or AFNO_ERR_HIP.  Not for concurrent use with calls on other streams.
+ */
+int afno_profile_begin(int max_calls);
+int afno_profile_end(double* kernel_ms, int64_t* calls);
+
+/* Message of the calling thread's last non-OK return ("" if none).  The pointer
+ * stays valid until the thread's next call into the library. */
+const char* afno_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int afno_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AFNO_H_ */

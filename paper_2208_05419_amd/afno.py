@@ -1,0 +1,172 @@
+"""Python binding of the C ABI in include/afno.h (argument marshalling only).
+
+Every step of the filter runs in the HIP kernels of ``libafno_mi355x.so``; this module
+only turns torch tensors into pointers, sizes and the current HIP stream.  There is no
+fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libafno_mi355x.so")
+
+AFNO_OK = 0
+AFNO_ERR_INVALID_ARG = -1
+AFNO_ERR_UNSUPPORTED = -2
+AFNO_ERR_ALIAS = -3
+AFNO_ERR_HIP = -4
+AFNO_DTYPE_FP32 = 0
+AFNO_DTYPE_BF16 = 1
+AFNO_STAGE_SPECTRUM = 1
+AFNO_STAGE_MIXED = 2
+AFNO_STAGE_DELTA = 3
+
+EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_profile_begin", "afno_profile_end",
+            "afno_last_error", "afno_version")
+KERNELS = ("row_r2c", "column", "row_c2r")
+
+_ERR_NAMES = {AFNO_ERR_INVALID_ARG: "AFNO_ERR_INVALID_ARG", AFNO_ERR_UNSUPPORTED: "AFNO_ERR_UNSUPPORTED",
+              AFNO_ERR_ALIAS: "AFNO_ERR_ALIAS", AFNO_ERR_HIP: "AFNO_ERR_HIP"}
+
+_lib = None
+
+
+class AfnoError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def load_library():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"AFNO HIP library not built: {LIB_PATH} is missing "
+                           "(run `python -c 'import __graft_entry__ as g; g.build()'`)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, vp, f32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
+    lib.afno_filter_forward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
+                                        ctypes.c_int, vp, vp]
+    lib.afno_filter_forward.restype = ctypes.c_int
+    lib.afno_filter_stage.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
+                                      ctypes.c_int, ctypes.c_int, vp, vp]
+    lib.afno_filter_stage.restype = ctypes.c_int
+    lib.afno_last_error.argtypes = []
+    lib.afno_last_error.restype = ctypes.c_char_p
+    lib.afno_version.argtypes = []
+    lib.afno_version.restype = ctypes.c_int
+    lib.afno_profile_begin.argtypes = [ctypes.c_int]
+    lib.afno_profile_begin.restype = ctypes.c_int
+    lib.afno_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+    lib.afno_profile_end.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def afno_last_error() -> str:
+    return load_library().afno_last_error().decode()
+
+
+def afno_version() -> int:
+    return int(load_library().afno_version())
+
+
+def _check(rc: int):
+    if rc != AFNO_OK:
+        raise AfnoError(rc, afno_last_error())
+
+
+def afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fraction, dtype,
+                        out, stream) -> int:
+    """Raw call: pointers as ints (or None), returns the C return code."""
+    return load_library().afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam,
+                                              keep_fraction, dtype, out, stream)
+
+
+def afno_filter_stage(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fraction, dtype,
+                      stage, dst, stream) -> int:
+    return load_library().afno_filter_stage(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam,
+                                            keep_fraction, dtype, stage, dst, stream)
+
+
+def afno_profile_begin(max_calls: int) -> int:
+    return load_library().afno_profile_begin(max_calls)
+
+
+def afno_profile_end(kernel_ms, calls) -> int:
+    return load_library().afno_profile_end(kernel_ms, calls)
+
+
+def profile_begin(max_calls: int):
+    _check(afno_profile_begin(max_calls))
+
+
+def profile_end():
+    """-> ({kernel name: summed ms}, timed calls)"""
+    ms = (ctypes.c_double * 3)()
+    calls = ctypes.c_int64()
+    _check(afno_profile_end(ms, ctypes.byref(calls)))
+    return dict(zip(KERNELS, list(ms))), int(calls.value)
+
+
+# ---------------------------------------------------------------- torch-level wrappers
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return AFNO_DTYPE_FP32
+    if t.dtype == torch.bfloat16:
+        return AFNO_DTYPE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    if not t.is_cuda:
+        raise ValueError("tensors must be on the GPU")
+    return t.data_ptr() or None
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction: float = 1.0,
+                   out=None, stream=None):
+    """out = x + AFNO filter(x) for x [B,H,W,C] (float32 or bfloat16 on the GPU);
+    weights w1 [nb,bs,bs,2], b1 [nb,bs,2], w2 [nb,bs,bs,2], b2 [nb,bs,2] of x's dtype.
+    Enqueued on ``stream`` (default: torch's current stream)."""
+    import torch
+    B, H, W, C = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    rc = afno_filter_forward(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W, C,
+                             num_blocks, lam, keep_fraction, _dtype_code(x), _ptr(out),
+                             _stream(stream))
+    _check(rc)
+    return out
+
+
+def filter_stage(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction: float, stage: int,
+                 stream=None):
+    """Diagnostic stage output in float32: spectrum / mixed spectrum [B,H,W/2+1,C,2] or the
+    filter output before the residual [B,H,W,C]."""
+    import torch
+    B, H, W, C = x.shape
+    shape = (B, H, W, C) if stage == AFNO_STAGE_DELTA else (B, H, W // 2 + 1, C, 2)
+    dst = torch.empty(shape, dtype=torch.float32, device=x.device)
+    rc = afno_filter_stage(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W, C,
+                           num_blocks, lam, keep_fraction, _dtype_code(x), stage, _ptr(dst),
+                           _stream(stream))
+    _check(rc)
+    return dst

@@ -1,0 +1,293 @@
+// afno_api.cpp -- the C ABI declared in include/afno.h: argument validation, the launch
+// plan (transform factorisation, cutoff counts, LDS budgets) and the stream-ordered
+// spectrum workspace.  Every step of the filter runs in the kernels of afno_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "afno.h"
+#include "afno_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+// n = 4^a 2^b 3^c 5^d -> one pass per factor; false if another prime divides n.
+bool factorize(int64_t n, afno::Radices& r) {
+  r.n = (int)n;
+  r.count = 0;
+  const int order[4] = {4, 2, 3, 5};
+  for (int f : order) {
+    while (n % f == 0 && (f != 2 || n % 4 != 0)) {
+      if (r.count >= afno::kMaxPasses) return false;
+      r.r[r.count++] = f;
+      n /= f;
+    }
+  }
+  return n == 1;
+}
+
+// every pass of `r` fits the per-thread register budget with nsub butterfly slots
+bool passes_fit(const afno::Radices& r, int nsub, int emax) {
+  for (int p = 0; p < r.count; ++p) {
+    const int R = r.r[p];
+    const int per_thread = (r.n / R + nsub - 1) / nsub;
+    if (per_thread > (emax + R - 1) / R) return false;
+  }
+  return true;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct Args {
+  const void *x, *w1, *b1, *w2, *b2;
+  int64_t B, H, W, C, nb;
+  float lam, keep;
+  int dtype;
+  void* out;
+  size_t out_bytes;  // 0: the size of x
+};
+
+// Validation (no HIP call) and plan construction.  Returns AFNO_OK, or an error code
+// with g_last_error set.
+int make_plan(const Args& a, afno::Plan& pl) {
+  if (a.dtype != AFNO_DTYPE_FP32 && a.dtype != AFNO_DTYPE_BF16)
+    return fail(AFNO_ERR_INVALID_ARG, "dtype must be AFNO_DTYPE_FP32 (0) or AFNO_DTYPE_BF16 (1)");
+  if (a.B < 0 || a.H <= 0 || a.W <= 0 || a.C <= 0 || a.nb <= 0)
+    return fail(AFNO_ERR_INVALID_ARG, "B must be >= 0 and H, W, C, num_blocks > 0");
+  if (a.C % a.nb != 0)
+    return fail(AFNO_ERR_INVALID_ARG, "C must be a multiple of num_blocks");
+  if (!std::isfinite(a.lam) || a.lam < 0.f)
+    return fail(AFNO_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+  if (!(a.keep > 0.f && a.keep <= 1.f))
+    return fail(AFNO_ERR_INVALID_ARG, "keep_fraction must be in (0, 1]");
+
+  pl.B = a.B; pl.H = a.H; pl.W = a.W; pl.C = a.C; pl.nb = a.nb;
+  pl.bs = a.C / a.nb;
+  pl.dtype = a.dtype;
+  // hard mode cutoff, products in double
+  const int64_t Kh = a.H / 2 + 1, Wm = a.W / 2 + 1;
+  pl.kept_h = (int64_t)std::floor((double)Kh * (double)a.keep);
+  pl.KW = (int64_t)std::floor((double)Wm * (double)a.keep);
+  if (pl.kept_h == 0) pl.KW = 0;  // no row passes: no mode is kept
+  if (a.B == 0) return AFNO_OK;
+
+  if (!a.x || !a.w1 || !a.b1 || !a.w2 || !a.b2 || !a.out)
+    return fail(AFNO_ERR_INVALID_ARG, "null pointer argument");
+
+  const size_t es = a.dtype == AFNO_DTYPE_FP32 ? 4 : 2;
+  if (!aligned(a.x, 16) || !aligned(a.out, 16))
+    return fail(AFNO_ERR_UNSUPPORTED, "x and out must be 16-byte aligned");
+  if (!aligned(a.w1, 4) || !aligned(a.b1, 4) || !aligned(a.w2, 4) || !aligned(a.b2, 4))
+    return fail(AFNO_ERR_UNSUPPORTED, "weights and biases must be 4-byte aligned");
+  if (a.W % 2 != 0) return fail(AFNO_ERR_UNSUPPORTED, "W must be even");
+  if (!factorize(a.W, pl.row.rw) || !factorize(a.H, pl.col.rh))
+    return fail(AFNO_ERR_UNSUPPORTED, "H and W must be of the form 2^a 3^b 5^c");
+  if (pl.bs % 16 != 0 || pl.bs > 128)
+    return fail(AFNO_ERR_UNSUPPORTED, "block size C/num_blocks must be a multiple of 16 and <= 128");
+  if (a.W > 1024) return fail(AFNO_ERR_UNSUPPORTED, "W must be <= 1024");
+  if (a.H > 16 * afno::kColMaxMTiles)
+    return fail(AFNO_ERR_UNSUPPORTED, "H must be <= 192");
+  const double elems = (double)a.B * a.H * a.W * a.C;
+  if (elems > 4.0e15 || (double)a.B * a.H > 2.0e9 || (double)a.B * Wm * a.nb > 2.0e9)
+    return fail(AFNO_ERR_UNSUPPORTED, "tensor too large");
+
+  // W-axis workgroups: rc channels, rc/2 complex signals
+  pl.row.W = (int)a.W; pl.row.C = (int)a.C; pl.row.KW = (int)pl.KW;
+  pl.row.inv_sqrt_w = (float)(1.0 / std::sqrt((double)a.W));
+  pl.row.rc = 0;
+  for (int rc : {64, 32, 16}) {
+    if (a.C % rc != 0) continue;
+    const int np = rc / 2;
+    const size_t lds = (size_t)a.W * np * 8 + (size_t)a.W * 8;
+    if (lds > (size_t)afno::kRowLdsMax) continue;
+    if (!passes_fit(pl.row.rw, afno::kRowThreads / np, afno::kRowEmax)) continue;
+    pl.row.rc = rc;
+    pl.row_lds = lds;
+    break;
+  }
+  if (pl.row.rc == 0) return fail(AFNO_ERR_UNSUPPORTED, "W too large for the W-axis kernel");
+
+  // column workgroups
+  afno::ColParams& c = pl.col;
+  c.H = (int)a.H; c.H16 = (int)((a.H + 15) / 16 * 16); c.bs = (int)pl.bs; c.nb = (int)a.nb;
+  c.C = (int)a.C; c.KW = (int)pl.KW; c.kept_h = (int)pl.kept_h;
+  c.lam = a.lam;
+  c.inv_sqrt_h = (float)(1.0 / std::sqrt((double)a.H));
+  c.ldt = 2 * c.bs + (a.dtype == AFNO_DTYPE_BF16 ? 8 : 4);
+  c.chk = (c.bs % 32 == 0) ? 32 : 16;  // must divide bs
+  pl.col_threads = 64 * (c.bs / 16 > 4 ? c.bs / 16 : 4);
+  c.tile_bytes = (int)(((size_t)c.H16 * c.ldt * es + 15) / 16 * 16);
+  pl.col_lds = (size_t)c.tile_bytes + (size_t)a.H * c.chk * 8 + (size_t)a.H * 8;
+  if (pl.col_lds > (size_t)afno::kLdsBytes)
+    return fail(AFNO_ERR_UNSUPPORTED, "column tile (H x block size) does not fit in LDS");
+  if (!passes_fit(c.rh, pl.col_threads / c.chk, afno::kColEmax))
+    return fail(AFNO_ERR_UNSUPPORTED, "H transform exceeds the per-thread register budget");
+
+  pl.spec_bytes = (size_t)a.B * a.H * pl.KW * a.C * 2 * es;
+
+  // out must not overlap any input
+  const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;
+  const size_t ob = a.out_bytes ? a.out_bytes : xb;
+  const size_t wb = (size_t)a.nb * pl.bs * pl.bs * 2 * es, bb = (size_t)a.nb * pl.bs * 2 * es;
+  if (overlaps(a.out, ob, a.x, xb) || overlaps(a.out, ob, a.w1, wb) ||
+      overlaps(a.out, ob, a.w2, wb) || overlaps(a.out, ob, a.b1, bb) ||
+      overlaps(a.out, ob, a.b2, bb))
+    return fail(AFNO_ERR_ALIAS, "out overlaps an input");
+  return AFNO_OK;
+}
+
+std::once_flag g_attr_once;
+
+// diagnostic per-kernel timing (afno_profile_begin / afno_profile_end)
+struct Profile {
+  std::mutex mu;
+  bool on = false;
+  int cap = 0, used = 0;
+  std::vector<hipEvent_t> ev;  // 4 per timed call
+};
+Profile g_prof;
+
+hipEvent_t* profile_slot() {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.used >= g_prof.cap) return nullptr;
+  return &g_prof.ev[4 * (size_t)g_prof.used++];
+}
+
+int run(const Args& a, int stage, float* dst, hipStream_t stream) {
+  afno::Plan pl;
+  int rc = make_plan(a, pl);
+  if (rc != AFNO_OK || a.B == 0) return rc;
+
+  std::call_once(g_attr_once, [] {
+    (void)afno::set_kernel_attributes();
+    (void)hipGetLastError();
+  });
+
+  const size_t xb = (size_t)a.B * a.H * a.W * a.C * (a.dtype == AFNO_DTYPE_FP32 ? 4 : 2);
+  hipError_t e;
+  if (pl.KW == 0) {  // nothing kept: the filter is zero
+    if (stage == afno::kStageFull)
+      e = hipMemcpyAsync(a.out, a.x, xb, hipMemcpyDeviceToDevice, stream);
+    else {
+      const size_t n = stage == afno::kStageDelta ? (size_t)a.B * a.H * a.W * a.C
+                                                  : (size_t)a.B * a.H * (a.W / 2 + 1) * a.C * 2;
+      e = hipMemsetAsync(dst, 0, n * sizeof(float), stream);
+    }
+    if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("copy: ") + hipGetErrorString(e));
+    return AFNO_OK;
+  }
+
+  void* S = nullptr;
+  e = hipMallocAsync(&S, pl.spec_bytes, stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") +
+                                  std::to_string(pl.spec_bytes) + " bytes: " + hipGetErrorString(e));
+  }
+  hipEvent_t* ev = stage == afno::kStageFull ? profile_slot() : nullptr;
+  e = afno::launch_filter(pl, a.x, a.w1, a.b1, a.w2, a.b2, S, a.out, dst, stage, stream, ev);
+  hipError_t ef = hipFreeAsync(S, stream);
+  if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
+  if (ef != hipSuccess) return fail(AFNO_ERR_HIP, std::string("workspace free: ") + hipGetErrorString(ef));
+  return AFNO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int afno_filter_forward(const void* x, const void* w1, const void* b1, const void* w2,
+                        const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                        int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                        void* out, hipStream_t stream) {
+  g_last_error.clear();
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0};
+  return run(a, afno::kStageFull, nullptr, stream);
+}
+
+int afno_filter_stage(const void* x, const void* w1, const void* b1, const void* w2,
+                      const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                      int64_t num_blocks, float lambda, float keep_fraction, int dtype, int stage,
+                      float* dst, hipStream_t stream) {
+  g_last_error.clear();
+  if (stage != AFNO_STAGE_SPECTRUM && stage != AFNO_STAGE_MIXED && stage != AFNO_STAGE_DELTA)
+    return fail(AFNO_ERR_INVALID_ARG, "stage must be AFNO_STAGE_SPECTRUM, _MIXED or _DELTA");
+  if (B > 0 && dst && !aligned(dst, 16))
+    return fail(AFNO_ERR_UNSUPPORTED, "dst must be 16-byte aligned");
+  // dst plays the part of out: it must not overlap an input either
+  const size_t nd = stage == AFNO_STAGE_DELTA ? (size_t)B * H * W * C
+                                              : (size_t)B * H * (W / 2 + 1) * C * 2;
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, dst,
+         B > 0 && H > 0 && W > 0 && C > 0 ? nd * sizeof(float) : 0};
+  return run(a, stage, dst, stream);
+}
+
+int afno_profile_begin(int max_calls) {
+  g_last_error.clear();
+  if (max_calls <= 0) return fail(AFNO_ERR_INVALID_ARG, "max_calls must be > 0");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.assign(4 * (size_t)max_calls, nullptr);
+  for (hipEvent_t& e : g_prof.ev) {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      for (hipEvent_t f : g_prof.ev)
+        if (f) (void)hipEventDestroy(f);
+      g_prof.ev.clear();
+      g_prof.on = false;
+      return fail(AFNO_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(r));
+    }
+  }
+  g_prof.cap = max_calls;
+  g_prof.used = 0;
+  g_prof.on = true;
+  return AFNO_OK;
+}
+
+int afno_profile_end(double* kernel_ms, int64_t* calls) {
+  g_last_error.clear();
+  if (!kernel_ms || !calls) return fail(AFNO_ERR_INVALID_ARG, "null output pointer");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on) return fail(AFNO_ERR_INVALID_ARG, "afno_profile_end without afno_profile_begin");
+  int rc = AFNO_OK;
+  double sum[3] = {0.0, 0.0, 0.0};
+  for (int c = 0; c < g_prof.used && rc == AFNO_OK; ++c) {
+    hipEvent_t* ev = &g_prof.ev[4 * (size_t)c];
+    hipError_t r = hipEventSynchronize(ev[3]);
+    for (int k = 0; k < 3 && r == hipSuccess; ++k) {
+      float ms = 0.f;
+      r = hipEventElapsedTime(&ms, ev[k], ev[k + 1]);
+      sum[k] += ms;
+    }
+    if (r != hipSuccess) rc = fail(AFNO_ERR_HIP, std::string("profile events: ") + hipGetErrorString(r));
+  }
+  for (int k = 0; k < 3; ++k) kernel_ms[k] = sum[k];
+  *calls = g_prof.used;
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.on = false;
+  g_prof.cap = g_prof.used = 0;
+  return rc;
+}
+
+const char* afno_last_error(void) { return g_last_error.c_str(); }
+
+int afno_version(void) { return 100; }
+
+}  // extern "C"

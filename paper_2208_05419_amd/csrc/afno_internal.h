@@ -1,0 +1,58 @@
+// afno_internal.h -- launch plan shared by the C ABI (afno_api.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fft_lds.h"
+
+namespace afno {
+
+constexpr int kRowThreads = 256;      // threads of a W-axis workgroup
+constexpr int kRowEmax = 32;          // complex values a thread holds in a W pass
+constexpr int kRowLdsMax = 160 * 1024; // LDS budget of a W-axis workgroup
+constexpr int kColEmax = 24;          // complex values a thread holds in an H pass
+constexpr int kColMaxMTiles = 12;     // 16-row MFMA tiles per column: H <= 192
+constexpr int kColMaxThreads = 512;   // 8 waves: bs <= 128
+constexpr int kLdsBytes = 160 * 1024; // LDS of one gfx950 CU
+
+constexpr int kStageFull = 0;
+constexpr int kStageSpectrum = 1;
+constexpr int kStageMixed = 2;
+constexpr int kStageDelta = 3;
+
+struct RowParams {
+  int W, C, KW, rc;   // rc channels (rc/2 complex signals) per workgroup
+  float inv_sqrt_w;
+  Radices rw;
+};
+
+struct ColParams {
+  int H, H16, bs, nb, C, KW;
+  int ldt;            // LDS row stride of the column tile, elements
+  int chk;            // channels per pass of the H transform
+  int kept_h;
+  int tile_bytes;
+  float lam, inv_sqrt_h;
+  Radices rh;
+};
+
+struct Plan {
+  int64_t B, H, W, C, nb, bs;
+  int dtype;          // 0 fp32, 1 bf16
+  int64_t KW;         // kept_w: W columns that carry kept modes
+  int64_t kept_h;
+  RowParams row;
+  ColParams col;
+  size_t row_lds, col_lds;
+  int col_threads;
+  size_t spec_bytes;  // workspace: B * H * KW * C complex values
+};
+
+hipError_t set_kernel_attributes();
+// ev: NULL, or 4 events recorded before the first kernel and after each of the three
+hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
+                         const void* w2, const void* b2, void* S, void* out, float* dst,
+                         int stage, hipStream_t st, hipEvent_t* ev);
+
+}  // namespace afno

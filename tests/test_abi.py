@@ -1,0 +1,115 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the header
+declares, and rejects bad arguments before any HIP call (validation runs first, so
+these calls never reach the device).  Pointers here are fake, aligned integers."""
+import math
+import os
+import re
+
+import pytest
+
+import paper_2208_05419_amd as afno
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# fake device addresses, 256-byte aligned and far apart
+X, W1, B1, W2, B2, OUT = (0x10000000 * (i + 1) for i in range(6))
+
+
+def _header_functions():
+    with open(os.path.join(ROOT, "include", "afno.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(afno_\w+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_header_symbols():
+    lib = afno.load_library()
+    names = _header_functions()
+    assert set(names) == set(afno.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version():
+    assert afno.afno_version() == 100
+
+
+def call(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, B=1, H=16, W=32, C=64, nb=4, lam=0.01, keep=1.0,
+             dtype=afno.AFNO_DTYPE_FP32, out=OUT, stream=None)
+    a.update(kw)
+    return afno.afno_filter_forward(a["x"], a["w1"], a["b1"], a["w2"], a["b2"], a["B"], a["H"],
+                                    a["W"], a["C"], a["nb"], a["lam"], a["keep"], a["dtype"],
+                                    a["out"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [
+    dict(x=None), dict(w1=None), dict(b1=None), dict(w2=None), dict(b2=None), dict(out=None),
+    dict(H=0), dict(W=-2), dict(C=0), dict(nb=0), dict(B=-1), dict(C=64, nb=3),
+    dict(lam=-0.1), dict(lam=math.nan), dict(lam=math.inf), dict(keep=0.0), dict(keep=1.5),
+    dict(keep=math.nan), dict(keep=-0.5), dict(dtype=2), dict(dtype=-1),
+])
+def test_invalid_arguments(kw):
+    assert call(**kw) == afno.AFNO_ERR_INVALID_ARG
+    assert afno.afno_last_error() != ""
+
+
+@pytest.mark.parametrize("kw", [
+    dict(H=7), dict(W=14), dict(W=33), dict(H=11, W=22),          # not 2,3,5-smooth / odd W
+    dict(C=96, nb=4),                                              # bs = 24, not a multiple of 16
+    dict(C=512, nb=2),                                             # bs = 256 > 128
+    dict(H=256),                                                   # H > 192
+    dict(W=2048),                                                  # W > 1024
+    dict(x=X + 8), dict(out=OUT + 4), dict(w1=W1 + 2),             # misaligned
+    dict(dtype=afno.AFNO_DTYPE_FP32, H=192, W=64, C=256, nb=2),   # fp32 tile 192 x 128 over LDS
+])
+def test_unsupported(kw):
+    assert call(**kw) == afno.AFNO_ERR_UNSUPPORTED
+    assert afno.afno_last_error() != ""
+
+
+@pytest.mark.parametrize("kw", [
+    dict(out=X), dict(out=X + 16 * 32 * 64 * 4 - 16), dict(out=W1), dict(out=B2 - 16),
+    dict(out=X - 16),
+])
+def test_alias(kw):
+    assert call(**kw) == afno.AFNO_ERR_ALIAS
+
+
+def test_batch_zero_is_ok_without_gpu():
+    assert call(B=0, x=None, out=None) == afno.AFNO_OK
+    assert afno.afno_last_error() == ""
+
+
+def test_batch_zero_still_validates_scalars():
+    assert call(B=0, C=64, nb=3) == afno.AFNO_ERR_INVALID_ARG
+
+
+def test_stage_validation():
+    f = afno.afno_filter_stage
+    assert f(X, W1, B1, W2, B2, 1, 16, 32, 64, 4, 0.01, 1.0, 0, 9, OUT, None) == afno.AFNO_ERR_INVALID_ARG
+    assert f(X, W1, B1, W2, B2, 1, 16, 32, 64, 4, 0.01, 1.0, 0, afno.AFNO_STAGE_DELTA, X,
+             None) == afno.AFNO_ERR_ALIAS
+    assert f(X, W1, B1, W2, B2, 1, 16, 32, 64, 4, 0.01, 1.0, 0, afno.AFNO_STAGE_SPECTRUM,
+             OUT + 8, None) == afno.AFNO_ERR_UNSUPPORTED
+
+
+def test_error_message_is_thread_local_and_cleared():
+    import threading
+    assert call(H=0) == afno.AFNO_ERR_INVALID_ARG
+    msgs = []
+    t = threading.Thread(target=lambda: msgs.append(afno.afno_last_error()))
+    t.start()
+    t.join()
+    assert msgs == [""]
+    assert afno.afno_last_error() != ""
+    assert call(B=0) == afno.AFNO_OK
+    assert afno.afno_last_error() == ""
+
+
+def test_missing_library_raises(monkeypatch, tmp_path):
+    import paper_2208_05419_amd.afno as mod
+    monkeypatch.setattr(mod, "_lib", None)
+    monkeypatch.setattr(mod, "LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        mod.load_library()
