@@ -118,6 +118,17 @@ int afno_filter_stage(const void* x, const void* w1, const void* b1, const void*
 int afno_profile_begin(int max_calls);
 int afno_profile_end(double* kernel_ms, int64_t* calls);
 
+/*
+ * Diagnostic kernel selection, process-wide.  AFNO_PATH_AUTO (the default) runs the
+ * size-specialised kernels where the library has them (W in {32, 180, 360}; H x bs in
+ * {16 x 16, 90 x 96, 180 x 128 (bf16)}) and the size-generic kernels elsewhere;
+ * AFNO_PATH_GENERIC runs the size-generic kernels for every shape.  Both compute the
+ * same filter.  Returns AFNO_OK or AFNO_ERR_INVALID_ARG.  Not for use while calls are
+ * being enqueued from other threads.
+ */
+enum { AFNO_PATH_AUTO = 0, AFNO_PATH_GENERIC = 1 };
+int afno_set_kernel_path(int path);
+
 /* Message of the calling thread's last non-OK return ("" if none).  The pointer
  * stays valid until the thread's next call into the library. */
 const char* afno_last_error(void);

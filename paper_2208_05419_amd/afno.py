@@ -23,8 +23,11 @@ AFNO_STAGE_SPECTRUM = 1
 AFNO_STAGE_MIXED = 2
 AFNO_STAGE_DELTA = 3
 
+AFNO_PATH_AUTO = 0
+AFNO_PATH_GENERIC = 1
+
 EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_profile_begin", "afno_profile_end",
-            "afno_last_error", "afno_version")
+            "afno_set_kernel_path", "afno_last_error", "afno_version")
 KERNELS = ("row_r2c", "column", "row_c2r")
 
 _ERR_NAMES = {AFNO_ERR_INVALID_ARG: "AFNO_ERR_INVALID_ARG", AFNO_ERR_UNSUPPORTED: "AFNO_ERR_UNSUPPORTED",
@@ -63,6 +66,8 @@ def load_library():
     lib.afno_profile_begin.restype = ctypes.c_int
     lib.afno_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     lib.afno_profile_end.restype = ctypes.c_int
+    lib.afno_set_kernel_path.argtypes = [ctypes.c_int]
+    lib.afno_set_kernel_path.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -99,6 +104,15 @@ def afno_profile_begin(max_calls: int) -> int:
 
 def afno_profile_end(kernel_ms, calls) -> int:
     return load_library().afno_profile_end(kernel_ms, calls)
+
+
+def afno_set_kernel_path(path: int) -> int:
+    return load_library().afno_set_kernel_path(path)
+
+
+def set_kernel_path(path: int):
+    """AFNO_PATH_AUTO: size-specialised kernels where available; AFNO_PATH_GENERIC: generic only."""
+    _check(afno_set_kernel_path(path))
 
 
 def profile_begin(max_calls: int):

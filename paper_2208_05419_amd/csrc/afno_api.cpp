@@ -286,6 +286,14 @@ int afno_profile_end(double* kernel_ms, int64_t* calls) {
   return rc;
 }
 
+int afno_set_kernel_path(int path) {
+  g_last_error.clear();
+  if (path != AFNO_PATH_AUTO && path != AFNO_PATH_GENERIC)
+    return fail(AFNO_ERR_INVALID_ARG, "path must be AFNO_PATH_AUTO or AFNO_PATH_GENERIC");
+  afno::set_kernel_path(path);
+  return AFNO_OK;
+}
+
 const char* afno_last_error(void) { return g_last_error.c_str(); }
 
 int afno_version(void) { return 100; }

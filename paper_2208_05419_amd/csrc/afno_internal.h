@@ -50,6 +50,9 @@ struct Plan {
 };
 
 hipError_t set_kernel_attributes();
+void set_kernel_path(int path);  // 0: size-specialised kernels where available, 1: generic only
+bool fast_row_available(int64_t W, int64_t C);
+bool fast_col_available(int dtype, int64_t H, int64_t bs);
 // ev: NULL, or 4 events recorded before the first kernel and after each of the three
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,

@@ -1,4 +1,6 @@
-// afno_kernels.hip -- gfx950 kernels of the AFNO spectral filter.
+// afno_kernels.hip -- launch sequence of the AFNO spectral filter on gfx950: picks the
+// size-specialised kernels of kernels_fast.h where one exists for the grid, else the
+// size-generic kernels of kernels_generic.h.
 //
 // Three passes over HBM, all on one spectrum workspace S [B][H][KW][C] (complex,
 // (re, im) interleaved, stored in the filter's dtype; KW = kept_w columns):
@@ -20,422 +22,86 @@
 #include <algorithm>
 
 #include "afno_internal.h"
-#include "fft_lds.h"
+#include "kernels_fast.h"
+#include "kernels_generic.h"
 
 namespace afno {
 
-typedef __bf16 bf16;
-typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-// ------------------------------------------------------------------ storage helpers
-
-template <typename T> struct Store;
-template <> struct Store<float> {
-  static constexpr int kVec = 4;  // elements per 16-byte vector
-  __device__ static float to(float v) { return v; }
-};
-template <> struct Store<bf16> {
-  static constexpr int kVec = 8;
-  __device__ static bf16 to(float v) { return (bf16)v; }  // round to nearest even
-};
-__device__ __forceinline__ float ld_f(const float* p) { return *p; }
-__device__ __forceinline__ float ld_f(const bf16* p) { return (float)*p; }
-
-// 16-byte vector of T viewed as floats / bf16
-union V16 {
-  uint4 u;
-  float f[4];
-  bf16 h[8];
-};
-
-// ------------------------------------------------------------------ kernel 1: W-axis R2C
-
-// grid (B * H, C / rc), block kRowThreads.  LDS: W x (rc/2) float2 signals + W twiddles.
-template <typename T>
-__global__ void __launch_bounds__(kRowThreads)
-row_r2c_kernel(const T* __restrict__ x, T* __restrict__ S, RowParams p) {
-  extern __shared__ float4 smem_raw[];
-  float2* buf = reinterpret_cast<float2*>(smem_raw);
-  const int np = p.rc / 2;
-  float2* tw = buf + (size_t)p.W * np;
-  const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;  // b * H + h
-  const int c0 = blockIdx.y * p.rc;
-
-  make_twiddles(tw, p.W);  // synchronises
-
-  // load x[b][h][:][c0 : c0 + rc] as np complex signals of length W
-  constexpr int V = Store<T>::kVec;
-  const int vpr = p.rc / V;
-  const T* xr = x + row * p.W * p.C + c0;
-  for (int it = tid; it < p.W * vpr; it += blockDim.x) {
-    const int n = it / vpr, cv = it - n * vpr;
-    V16 v;
-    v.u = *reinterpret_cast<const uint4*>(xr + (int64_t)n * p.C + cv * V);
-#pragma unroll
-    for (int q = 0; q < V / 2; ++q) {
-      float a, b;
-      if constexpr (V == 4) { a = v.f[2 * q]; b = v.f[2 * q + 1]; }
-      else { a = (float)v.h[2 * q]; b = (float)v.h[2 * q + 1]; }
-      buf[n * np + cv * (V / 2) + q] = make_float2(a, b);
-    }
-  }
-  __syncthreads();
-
-  const int sig = tid % np, sub = tid / np, nsub = blockDim.x / np;
-  fft_lds<kRowEmax, false>(buf, np, p.rw, sig, sub, nsub, tw);
-
-  // separate the two real channels of each signal and store kw in [0, KW):
-  //   X_c = (Z[k] + conj Z[W-k]) / 2,  X_{c+1} = (Z[k] - conj Z[W-k]) / (2i)
-  const float sc = 0.5f * p.inv_sqrt_w;
-  T* Sr = S + row * (int64_t)p.KW * p.C * 2;
-  for (int it = tid; it < p.KW * np; it += blockDim.x) {
-    const int k = it / np, q = it - k * np;
-    const float2 z = buf[k * np + q];
-    const int km = (k == 0) ? 0 : p.W - k;
-    const float2 zm = buf[km * np + q];
-    const float ar = (z.x + zm.x) * sc, ai = (z.y - zm.y) * sc;
-    const float br = (z.y + zm.y) * sc, bi = (zm.x - z.x) * sc;
-    T* o = Sr + ((int64_t)k * p.C + c0 + 2 * q) * 2;
-    if constexpr (V == 4) {
-      *reinterpret_cast<float4*>(o) = make_float4(ar, ai, br, bi);
-    } else {
-      union { uint2 u; bf16 h[4]; } w;
-      w.h[0] = (bf16)ar; w.h[1] = (bf16)ai; w.h[2] = (bf16)br; w.h[3] = (bf16)bi;
-      *reinterpret_cast<uint2*>(o) = w.u;
-    }
-  }
+// ------------------------------------------------------------------ size-specialised dispatch
+//
+// W-axis kernels: W = N1 N2, NP complex signals (2 NP channels) per workgroup.
+//   W = 32: 8 x 4, NP 32;  W = 180: 12 x 15, NP 32;  W = 360: 24 x 15, NP 16.
+// Column kernel: H = N1 N2 with block size BS.
+//   H = 16, BS = 16: 4 x 4;  H = 90, BS = 96: 9 x 10;  H = 180, BS = 128: 12 x 15 (bf16 only,
+//   with a bf16 transform intermediate: a float one would not fit the LDS).
+#define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
+bool fast_row_available(int64_t W, int64_t C) {
+#define AFNO_CASE(w, n1, n2, np) if (W == w) return C % (2 * np) == 0;
+  AFNO_ROW_FAST_LIST(AFNO_CASE)
+#undef AFNO_CASE
+  return false;
 }
 
-// ------------------------------------------------------------------ kernel 3: W-axis C2R + residual
-
-// grid (B * H, C / rc), block kRowThreads.  mode 0: out = x + y in T; mode 1: dst = y (float).
-template <typename T>
-__global__ void __launch_bounds__(kRowThreads)
-row_c2r_kernel(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ out,
-               float* __restrict__ dst, RowParams p, int mode) {
-  extern __shared__ float4 smem_raw[];
-  float2* buf = reinterpret_cast<float2*>(smem_raw);
-  const int np = p.rc / 2;
-  float2* tw = buf + (size_t)p.W * np;
-  const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;  // b * H + h
-  const int c0 = blockIdx.y * p.rc;
-  const int half = p.W / 2;
-
-  make_twiddles(tw, p.W);
-
-  // Z[k] = Y_c[k] + i Y_{c+1}[k] over the full length, with Y[W-k] = conj Y[k] and only
-  // the real parts of the k = 0 and k = W/2 bins; columns k >= KW are zero.
-  const T* Sr = S + row * (int64_t)p.KW * p.C * 2;
-  for (int it = tid; it < (half + 1) * np; it += blockDim.x) {
-    const int k = it / np, q = it - k * np;
-    float ar = 0.f, ai = 0.f, br = 0.f, bi = 0.f;
-    if (k < p.KW) {
-      const T* s = Sr + ((int64_t)k * p.C + c0 + 2 * q) * 2;
-      if constexpr (Store<T>::kVec == 4) {
-        const float4 v = *reinterpret_cast<const float4*>(s);
-        ar = v.x; ai = v.y; br = v.z; bi = v.w;
-      } else {
-        union { uint2 u; bf16 h[4]; } w;
-        w.u = *reinterpret_cast<const uint2*>(s);
-        ar = (float)w.h[0]; ai = (float)w.h[1]; br = (float)w.h[2]; bi = (float)w.h[3];
-      }
-    }
-    if (k == 0 || k == half) {
-      buf[k * np + q] = make_float2(ar, br);
-    } else {
-      buf[k * np + q] = make_float2(ar - bi, ai + br);
-      buf[(p.W - k) * np + q] = make_float2(ar + bi, br - ai);
-    }
-  }
-  __syncthreads();
-
-  const int sig = tid % np, sub = tid / np, nsub = blockDim.x / np;
-  fft_lds<kRowEmax, true>(buf, np, p.rw, sig, sub, nsub, tw);
-
-  constexpr int V = Store<T>::kVec;
-  const int vpr = p.rc / V;
-  const float sc = p.inv_sqrt_w;
-  const int64_t base = row * p.W * p.C + c0;
-  for (int it = tid; it < p.W * vpr; it += blockDim.x) {
-    const int n = it / vpr, cv = it - n * vpr;
-    const int64_t off = base + (int64_t)n * p.C + cv * V;
-    float y[V];
-#pragma unroll
-    for (int q = 0; q < V / 2; ++q) {
-      const float2 z = buf[n * np + cv * (V / 2) + q];
-      y[2 * q] = z.x * sc;
-      y[2 * q + 1] = z.y * sc;
-    }
-    if (mode == 1) {
-#pragma unroll
-      for (int e = 0; e < V; e += 4)
-        *reinterpret_cast<float4*>(dst + off + e) = make_float4(y[e], y[e + 1], y[e + 2], y[e + 3]);
-      continue;
-    }
-    V16 xv, ov;
-    xv.u = *reinterpret_cast<const uint4*>(x + off);
-#pragma unroll
-    for (int e = 0; e < V; ++e) {
-      if constexpr (V == 4) ov.f[e] = xv.f[e] + y[e];
-      else ov.h[e] = (bf16)((float)xv.h[e] + y[e]);
-    }
-    *reinterpret_cast<uint4*>(out + off) = ov.u;
-  }
+bool fast_col_available(int dtype, int64_t H, int64_t bs) {
+  if ((H == 16 && bs == 16) || (H == 90 && bs == 96)) return true;
+  return dtype == 1 && H == 180 && bs == 128;
 }
 
-// ------------------------------------------------------------------ kernel 2: column
-
-// MFMA operand types per storage dtype.
-template <typename T> struct Mma;
-
-// bf16: v_mfma_f32_16x16x32_bf16.  Lane l: A row l%16, k 8(l/16)..+7; B column l%16,
-// k 8(l/16)..+7; D column l%16, rows 4(l/16)..+3.
-template <> struct Mma<bf16> {
-  static constexpr int kK = 32;
-  typedef bf16x8 Frag;
-  // A fragment: 8 consecutive bf16 of an LDS row.
-  __device__ static Frag load_a(const bf16* row, int kbase, int lane) {
-    return *reinterpret_cast<const bf16x8*>(row + kbase + 8 * (lane >> 4));
+template <typename T>
+static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, hipStream_t st) {
+  const unsigned gx = (unsigned)(pl.B * pl.H);
+  const float sc = 0.5f * pl.row.inv_sqrt_w;
+#define AFNO_CASE(w, n1, n2, np)                                                          \
+  if (pl.W == w) {                                                                        \
+    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(gx, (unsigned)(pl.C / (2 * np))), \
+                       dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc);            \
+    return;                                                                               \
   }
-  // B fragment of the real-ified complex weight at output column nu = 2j + sg:
-  //   Wexp[2i + rho][2j + sg] = (Wr, -Wi ; Wi, Wr)[rho][sg]
-  // w points at the block's [n_in][n_out][2] complex weights.
-  __device__ static Frag load_b(const bf16* w, int n_out, int kbase, int j, int sg, int lane) {
-    const int i0 = (kbase >> 1) + 4 * (lane >> 4);
-    const uint32_t* wp = reinterpret_cast<const uint32_t*>(w);
-    union { uint32_t u[4]; Frag f; } r;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t v = wp[(int64_t)(i0 + q) * n_out + j];  // lo = re, hi = im
-      r.u[q] = sg ? ((v >> 16) | (v << 16)) : (v ^ 0x80000000u);
-    }
-    return r.f;
-  }
-  __device__ static f32x4 mma(Frag a, Frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-};
-
-// fp32: v_mfma_f32_16x16x4_f32.  Lane l: A row l%16, k l/16; B column l%16, k l/16.
-template <> struct Mma<float> {
-  static constexpr int kK = 4;
-  typedef float Frag;
-  __device__ static Frag load_a(const float* row, int kbase, int lane) {
-    return row[kbase + (lane >> 4)];
-  }
-  __device__ static Frag load_b(const float* w, int n_out, int kbase, int j, int sg, int lane) {
-    const int kap = kbase + (lane >> 4);
-    const int i = kap >> 1, rho = kap & 1;
-    const float v = w[((int64_t)i * n_out + j) * 2 + (rho ^ sg)];
-    return (rho == 1 && sg == 0) ? -v : v;
-  }
-  __device__ static f32x4 mma(Frag a, Frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-  }
-};
-
-__device__ __forceinline__ bool row_kept(int r, int H, int kept_h) {
-  if (r >= H) return false;
-  int s = (r <= H / 2) ? r : r - H;
-  s = s < 0 ? -s : s;
-  return s < kept_h;
+  AFNO_ROW_FAST_LIST(AFNO_CASE)
+#undef AFNO_CASE
 }
 
-// One layer of the block MLP on the LDS tile: acc[m][n] = tile rows x Wexp for the
-// wave's two 16-column output tiles, over the live row tiles.
 template <typename T>
-__device__ __forceinline__ void block_gemm(const T* tile, int ldt, const T* w, int n_out,
-                                           int n_in, int mt, uint32_t live, int wave, int lane,
-                                           f32x4 (&acc)[kColMaxMTiles][2]) {
-  typedef Mma<T> M;
-#pragma unroll
-  for (int m = 0; m < kColMaxMTiles; ++m)
-    for (int n = 0; n < 2; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int jn0 = (32 * wave + (lane & 15)) >> 1;  // complex output column of tile 0
-  const int jn1 = jn0 + 8;
-  const int sg = lane & 1;
-  for (int kb = 0; kb < 2 * n_in; kb += M::kK) {
-    const typename M::Frag b0 = M::load_b(w, n_out, kb, jn0, sg, lane);
-    const typename M::Frag b1 = M::load_b(w, n_out, kb, jn1, sg, lane);
-#pragma unroll
-    for (int m = 0; m < kColMaxMTiles; ++m) {
-      if (m < mt && ((live >> m) & 1u)) {
-        const typename M::Frag a = M::load_a(tile + (16 * m + (lane & 15)) * ldt, kb, lane);
-        acc[m][0] = M::mma(a, b0, acc[m][0]);
-        acc[m][1] = M::mma(a, b1, acc[m][1]);
-      }
-    }
+static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, float* dst,
+                                int mode, hipStream_t st) {
+  const unsigned gx = (unsigned)(pl.B * pl.H);
+  const float sc = pl.row.inv_sqrt_w;
+#define AFNO_CASE(w, n1, n2, np)                                                          \
+  if (pl.W == w) {                                                                        \
+    hipLaunchKernelGGL((row_c2r_fast<T, w, n1, n2, np>), dim3(gx, (unsigned)(pl.C / (2 * np))), \
+                       dim3(np * n1), 0, st, S, x, out, dst, (int)pl.C, (int)pl.KW, sc, mode); \
+    return;                                                                               \
   }
+  AFNO_ROW_FAST_LIST(AFNO_CASE)
+#undef AFNO_CASE
 }
 
-// grid B * KW * nb, block 64 * max(bs / 16, 4).  stage: 0 full, 1 stop after the forward
-// transform, 2 stop after the MLP.
-template <typename T>
-__global__ void __launch_bounds__(kColMaxThreads)
-column_kernel(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b1,
-              const T* __restrict__ w2, const T* __restrict__ b2, ColParams p, int stage) {
-  extern __shared__ float4 smem_raw[];
-  T* tile = reinterpret_cast<T*>(smem_raw);                              // H16 x ldt
-  float2* fbuf = reinterpret_cast<float2*>(reinterpret_cast<char*>(smem_raw) + p.tile_bytes);
-  float2* tw = fbuf + (size_t)p.H * p.chk;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nthr = blockDim.x;
-  const int bs = p.bs, ldt = p.ldt, H = p.H, H16 = p.H16;
-
-  const int blk = blockIdx.x % p.nb;  // consecutive workgroups -> different XCDs -> blocks
-  const int rest = blockIdx.x / p.nb;
-  const int kw = rest % p.KW;
-  const int64_t b = rest / p.KW;
-
-  make_twiddles(tw, H);
-
-  // ---- load the column tile: rows h < H of S[b][h][kw][blk*bs : +bs], zero padding rows
-  constexpr int V = Store<T>::kVec;
-  const int vpr = 2 * bs / V;
-  const int64_t row_stride = (int64_t)p.KW * p.C * 2;
-  T* col = S + ((b * H) * p.KW + kw) * (int64_t)p.C * 2 + (int64_t)blk * bs * 2;
-  for (int it = tid; it < H16 * vpr; it += nthr) {
-    const int h = it / vpr, cv = it - h * vpr;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (h < H) v = *reinterpret_cast<const uint4*>(col + h * row_stride + cv * V);
-    *reinterpret_cast<uint4*>(tile + h * ldt + cv * V) = v;
-  }
-  __syncthreads();
-
-  const int chk = p.chk;
-  const int sig = tid % chk, sub = tid / chk, nsub = nthr / chk;
-  const float sch = p.inv_sqrt_h;
-
-  // ---- forward DFT along H, chk channels at a time through the float32 buffer
-  for (int cc = 0; cc < bs; cc += chk) {
-    for (int it = tid; it < H * chk; it += nthr) {
-      const int h = it / chk, q = it - h * chk;
-      const T* e = tile + h * ldt + 2 * (cc + q);
-      fbuf[h * chk + q] = make_float2(ld_f(e), ld_f(e + 1));
-    }
-    __syncthreads();
-    fft_lds<kColEmax, false>(fbuf, chk, p.rh, sig, sub, nsub, tw);
-    for (int it = tid; it < H * chk; it += nthr) {
-      const int h = it / chk, q = it - h * chk;
-      const float2 z = fbuf[h * chk + q];
-      T* e = tile + h * ldt + 2 * (cc + q);
-      e[0] = Store<T>::to(z.x * sch);
-      e[1] = Store<T>::to(z.y * sch);
-    }
-    __syncthreads();
-  }
-
-  if (stage != 1) {
-    // ---- block MLP.  Waves own 32 real output columns (16 complex) each.
-    const int nw_mma = bs / 16;
-    const int mt = H16 / 16;
-    uint32_t live = 0;
-    for (int m = 0; m < mt; ++m) {
-      bool any = false;
-      for (int r = 16 * m; r < 16 * m + 16; ++r) any |= row_kept(r, H, p.kept_h);
-      live |= (any ? 1u : 0u) << m;
-    }
-    const T* W1 = w1 + (int64_t)blk * bs * bs * 2;
-    const T* W2 = w2 + (int64_t)blk * bs * bs * 2;
-    const T* B1 = b1 + (int64_t)blk * bs * 2;
-    const T* B2 = b2 + (int64_t)blk * bs * 2;
-    const bool active = wave < nw_mma;
-    const int nu0 = 32 * wave + (lane & 15);  // real output column of tile 0 (tile 1: +16)
-    f32x4 acc[kColMaxMTiles][2];
-
-    if (active) block_gemm<T>(tile, ldt, W1, bs, bs, mt, live, wave, lane, acc);
-    __syncthreads();  // every wave has read the spectrum rows
-    if (active) {
-      const float bia0 = ld_f(B1 + nu0), bia1 = ld_f(B1 + nu0 + 16);
-#pragma unroll
-      for (int m = 0; m < kColMaxMTiles; ++m) {
-        if (m < mt && ((live >> m) & 1u)) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = 16 * m + 4 * (lane >> 4) + r;
-            tile[row * ldt + nu0] = Store<T>::to(fmaxf(acc[m][0][r] + bia0, 0.f));
-            tile[row * ldt + nu0 + 16] = Store<T>::to(fmaxf(acc[m][1][r] + bia1, 0.f));
-          }
-        }
-      }
-    }
-    __syncthreads();  // hidden layer complete
-    if (active) block_gemm<T>(tile, ldt, W2, bs, bs, mt, live, wave, lane, acc);
-    __syncthreads();  // every wave has read the hidden rows
-    if (active) {
-      const float bia0 = ld_f(B2 + nu0), bia1 = ld_f(B2 + nu0 + 16);
-      const float lam = p.lam;
-#pragma unroll
-      for (int m = 0; m < kColMaxMTiles; ++m) {
-        if (m < mt) {
-          const bool lv = (live >> m) & 1u;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = 16 * m + 4 * (lane >> 4) + r;
-            const bool keep = lv && row_kept(row, H, p.kept_h);
-            float o0 = lv ? acc[m][0][r] + bia0 : 0.f;
-            float o1 = lv ? acc[m][1][r] + bia1 : 0.f;
-            o0 = o0 > lam ? o0 - lam : (o0 < -lam ? o0 + lam : 0.f);
-            o1 = o1 > lam ? o1 - lam : (o1 < -lam ? o1 + lam : 0.f);
-            tile[row * ldt + nu0] = Store<T>::to(keep ? o0 : 0.f);
-            tile[row * ldt + nu0 + 16] = Store<T>::to(keep ? o1 : 0.f);
-          }
-        }
-      }
-    }
-    __syncthreads();
-
-    if (stage == 0) {
-      // ---- inverse DFT along H
-      for (int cc = 0; cc < bs; cc += chk) {
-        for (int it = tid; it < H * chk; it += nthr) {
-          const int h = it / chk, q = it - h * chk;
-          const T* e = tile + h * ldt + 2 * (cc + q);
-          fbuf[h * chk + q] = make_float2(ld_f(e), ld_f(e + 1));
-        }
-        __syncthreads();
-        fft_lds<kColEmax, true>(fbuf, chk, p.rh, sig, sub, nsub, tw);
-        for (int it = tid; it < H * chk; it += nthr) {
-          const int h = it / chk, q = it - h * chk;
-          const float2 z = fbuf[h * chk + q];
-          T* e = tile + h * ldt + 2 * (cc + q);
-          e[0] = Store<T>::to(z.x * sch);
-          e[1] = Store<T>::to(z.y * sch);
-        }
-        __syncthreads();
-      }
-    }
-  }
-
-  // ---- store the tile back in place
-  for (int it = tid; it < H * vpr; it += nthr) {
-    const int h = it / vpr, cv = it - h * vpr;
-    *reinterpret_cast<uint4*>(col + h * row_stride + cv * V) =
-        *reinterpret_cast<const uint4*>(tile + h * ldt + cv * V);
-  }
+template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE>
+static void launch_col_fast_one(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
+                                const T* b2, int stage, hipStream_t st) {
+  constexpr int lds = ColLds<T, FT, H, BS>::kBytes;
+  constexpr int nthr = ColShape<BS>::kThreads;
+  hipLaunchKernelGGL((column_fast<T, FT, H, N1, N2, BS, WPE>), dim3((unsigned)(pl.B * pl.KW * pl.nb)),
+                     dim3(nthr), lds, st, S, w1, b1, w2, b2, (int)pl.C, (int)pl.KW, (int)pl.nb,
+                     (int)pl.kept_h, pl.col.lam, pl.col.inv_sqrt_h, stage);
 }
 
-// ------------------------------------------------------------------ diagnostic export
-
-// dst [B][H][Wm][C][2] float from S [B][H][KW][C][2]; columns kw >= KW written as 0.
 template <typename T>
-__global__ void export_spectrum_kernel(const T* __restrict__ S, float* __restrict__ dst,
-                                       int64_t B, int H, int Wm, int KW, int C) {
-  const int64_t total = B * H * (int64_t)Wm * C * 2;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t e = i % (2 * C);
-    const int64_t r = i / (2 * C);  // (b * H + h) * Wm + kw
-    const int kw = (int)(r % Wm);
-    const int64_t bh = r / Wm;
-    dst[i] = (kw < KW) ? ld_f(S + (bh * KW + kw) * 2 * C + e) : 0.f;
-  }
+static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
+                            const T* b2, int stage, hipStream_t st) {
+  if (pl.H == 16 && pl.bs == 16)
+    launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, w1, b1, w2, b2, stage, st);
+  else if (pl.H == 90 && pl.bs == 96)
+    launch_col_fast_one<T, float, 90, 9, 10, 96, 3>(pl, S, w1, b1, w2, b2, stage, st);
+  else if constexpr (sizeof(T) == 2)
+    launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, w1, b1, w2, b2, stage, st);
 }
 
 // ------------------------------------------------------------------ launchers
+
+static int g_kernel_path = 0;  // 0: size-specialised where available, 1: generic only
+
+void set_kernel_path(int path) { g_kernel_path = path; }
 
 template <typename T>
 static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, const void* b1,
@@ -443,17 +109,27 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
                              int stage, hipStream_t st, hipEvent_t* ev) {
   const T* xt = static_cast<const T*>(x);
   T* St = static_cast<T*>(S);
+  const bool generic = g_kernel_path == 1;
+  const bool row_fast = !generic && fast_row_available(pl.W, pl.C);
+  const bool col_fast = !generic && fast_col_available(pl.dtype, pl.H, pl.bs);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
   if (ev) (void)hipEventRecord(ev[0], st);
-  hipLaunchKernelGGL(row_r2c_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, xt, St, pl.row);
+  if (row_fast)
+    launch_row_fwd_fast<T>(pl, xt, St, st);
+  else
+    hipLaunchKernelGGL(row_r2c_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, xt, St, pl.row);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], st);
   const int col_stage = (stage == kStageSpectrum) ? 1 : (stage == kStageMixed ? 2 : 0);
-  hipLaunchKernelGGL(column_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
-                     dim3(pl.col_threads), pl.col_lds, st, St, static_cast<const T*>(w1),
-                     static_cast<const T*>(b1), static_cast<const T*>(w2),
-                     static_cast<const T*>(b2), pl.col, col_stage);
+  if (col_fast)
+    launch_col_fast<T>(pl, St, static_cast<const T*>(w1), static_cast<const T*>(b1),
+                       static_cast<const T*>(w2), static_cast<const T*>(b2), col_stage, st);
+  else
+    hipLaunchKernelGGL(column_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
+                       dim3(pl.col_threads), pl.col_lds, st, St, static_cast<const T*>(w1),
+                       static_cast<const T*>(b1), static_cast<const T*>(w2),
+                       static_cast<const T*>(b2), pl.col, col_stage);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[2], st);
@@ -464,8 +140,12 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
                        (int)pl.H, (int)(pl.W / 2 + 1), (int)pl.KW, (int)pl.C);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, St, xt,
-                     static_cast<T*>(out), dst, pl.row, stage == kStageDelta ? 1 : 0);
+  const int mode = stage == kStageDelta ? 1 : 0;
+  if (row_fast)
+    launch_row_inv_fast<T>(pl, St, xt, static_cast<T*>(out), dst, mode, st);
+  else
+    hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, St, xt,
+                       static_cast<T*>(out), dst, pl.row, mode);
   e = hipGetLastError();
   if (ev && e == hipSuccess) (void)hipEventRecord(ev[3], st);
   return e;
@@ -473,19 +153,24 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
 
 hipError_t set_kernel_attributes() {
   const int lds_max = kLdsBytes;
-  hipError_t e;
+  hipError_t e, first = hipSuccess;
 #define AFNO_ATTR(K)                                                                         \
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(K),                                \
                           hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);            \
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess && first == hipSuccess) first = e;
   AFNO_ATTR(row_r2c_kernel<float>)
   AFNO_ATTR(row_r2c_kernel<bf16>)
   AFNO_ATTR(row_c2r_kernel<float>)
   AFNO_ATTR(row_c2r_kernel<bf16>)
   AFNO_ATTR(column_kernel<float>)
   AFNO_ATTR(column_kernel<bf16>)
+  AFNO_ATTR((column_fast<float, float, 16, 4, 4, 16, 4>))
+  AFNO_ATTR((column_fast<bf16, float, 16, 4, 4, 16, 4>))
+  AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 3>))
+  AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 3>))
+  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2>))
 #undef AFNO_ATTR
-  return hipSuccess;
+  return first;
 }
 
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,

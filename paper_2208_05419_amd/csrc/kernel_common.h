@@ -1,0 +1,129 @@
+// kernel_common.h -- storage types, MFMA operand helpers and the cutoff test shared by
+// the generic and the size-specialised kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace afno {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Store;
+template <> struct Store<float> {
+  static constexpr int kVec = 4;  // elements per 16-byte vector
+  __device__ static float to(float v) { return v; }
+};
+template <> struct Store<bf16> {
+  static constexpr int kVec = 8;
+  __device__ static bf16 to(float v) { return (bf16)v; }  // round to nearest even
+};
+__device__ __forceinline__ float ld_f(const float* p) { return *p; }
+__device__ __forceinline__ float ld_f(const bf16* p) { return (float)*p; }
+
+// 16-byte vector of T viewed as floats / bf16
+union V16 {
+  uint4 u;
+  float f[4];
+  bf16 h[8];
+};
+
+// One complex value (re, im) in storage type T.
+__device__ __forceinline__ float2 ld_c(const float* p) { return *reinterpret_cast<const float2*>(p); }
+__device__ __forceinline__ float2 ld_c(const bf16* p) {
+  union { uint32_t u; bf16 h[2]; } w;
+  w.u = *reinterpret_cast<const uint32_t*>(p);
+  return make_float2((float)w.h[0], (float)w.h[1]);
+}
+__device__ __forceinline__ void st_c(float* p, float2 v) { *reinterpret_cast<float2*>(p) = v; }
+__device__ __forceinline__ void st_c(bf16* p, float2 v) {
+  union { uint32_t u; bf16 h[2]; } w;
+  w.h[0] = (bf16)v.x;
+  w.h[1] = (bf16)v.y;
+  *reinterpret_cast<uint32_t*>(p) = w.u;
+}
+// Two complex values (4 T) in one access.
+__device__ __forceinline__ float4 ld_c2(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld_c2(const bf16* p) {
+  union { uint2 u; bf16 h[4]; } w;
+  w.u = *reinterpret_cast<const uint2*>(p);
+  return make_float4((float)w.h[0], (float)w.h[1], (float)w.h[2], (float)w.h[3]);
+}
+__device__ __forceinline__ void st_c2(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void st_c2(bf16* p, float4 v) {
+  union { uint2 u; bf16 h[4]; } w;
+  w.h[0] = (bf16)v.x; w.h[1] = (bf16)v.y; w.h[2] = (bf16)v.z; w.h[3] = (bf16)v.w;
+  *reinterpret_cast<uint2*>(p) = w.u;
+}
+
+// MFMA operand types per storage dtype.
+template <typename T> struct Mma;
+
+// bf16: v_mfma_f32_16x16x32_bf16.  Lane l: A row l%16, k 8(l/16)..+7; B column l%16,
+// k 8(l/16)..+7; D column l%16, rows 4(l/16)..+3.
+template <> struct Mma<bf16> {
+  static constexpr int kK = 32;
+  typedef bf16x8 Frag;
+  // A fragment: 8 consecutive bf16 of an LDS row.
+  __device__ static Frag load_a(const bf16* row, int kbase, int lane) {
+    return *reinterpret_cast<const bf16x8*>(row + kbase + 8 * (lane >> 4));
+  }
+  // B fragment of the real-ified complex weight at output column nu = 2j + sg:
+  //   Wexp[2i + rho][2j + sg] = (Wr, -Wi ; Wi, Wr)[rho][sg]
+  // w points at the block's [n_in][n_out][2] complex weights.  Each dword holds one
+  // complex weight (lo = re, hi = im); sg = 0 needs (re, -im), sg = 1 needs (im, re):
+  // a byte permutation and a sign flip with per-lane constants, so no lane diverges
+  // and all four loads are in flight before the first use.
+  __device__ static Frag load_b(const bf16* w, int n_out, int kbase, int j, int sg, int lane) {
+    const int i0 = (kbase >> 1) + 4 * (lane >> 4);
+    const uint32_t* wp = reinterpret_cast<const uint32_t*>(w) + (int64_t)i0 * n_out + j;
+    uint32_t v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = wp[(int64_t)q * n_out];
+    const uint32_t sel = sg ? 0x01000302u : 0x03020100u;
+    const uint32_t flip = sg ? 0u : 0x80000000u;
+    union { uint32_t u[4]; Frag f; } r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.u[q] = __builtin_amdgcn_perm(v[q], v[q], sel) ^ flip;
+    return r.f;
+  }
+  __device__ static f32x4 mma(Frag a, Frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+// fp32: v_mfma_f32_16x16x4_f32.  Lane l: A row l%16, k l/16; B column l%16, k l/16.
+template <> struct Mma<float> {
+  static constexpr int kK = 4;
+  typedef float Frag;
+  __device__ static Frag load_a(const float* row, int kbase, int lane) {
+    return row[kbase + (lane >> 4)];
+  }
+  // Wexp[2i + rho][2j + sg]: component rho ^ sg of w[i][j], negated for rho = 1, sg = 0
+  // (per-lane constants, no divergence).
+  __device__ static Frag load_b(const float* w, int n_out, int kbase, int j, int sg, int lane) {
+    const int kap = kbase + (lane >> 4);
+    const int i = kap >> 1, rho = kap & 1;
+    const float v = w[((int64_t)i * n_out + j) * 2 + (rho ^ sg)];
+    const uint32_t flip = (uint32_t)(rho & (sg ^ 1)) << 31;
+    return __uint_as_float(__float_as_uint(v) ^ flip);
+  }
+  __device__ static f32x4 mma(Frag a, Frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+// hard mode cutoff along H: row kh kept when |signed kh| < kept_h
+__device__ __forceinline__ bool row_kept(int r, int H, int kept_h) {
+  if (r >= H) return false;
+  int s = (r <= H / 2) ? r : r - H;
+  s = s < 0 ? -s : s;
+  return s < kept_h;
+}
+
+__device__ __forceinline__ float softshrink(float v, float lam) {
+  return v > lam ? v - lam : (v < -lam ? v + lam : 0.f);
+}
+
+}  // namespace afno

@@ -1,0 +1,433 @@
+// kernels_fast.h -- size-specialised kernels of the AFNO filter.
+//
+// The same three HBM passes as kernels_generic.h, with every transform length fixed
+// at compile time and split as N = N1 * N2 into two register-resident DFT stages
+// (dft_reg.h) around one exchange through LDS:
+//   n = n1 + N1 n2, k = k2 + N2 k1:
+//   X[k2 + N2 k1] = sum_n1 w_N1^(n1 k1) [ w_N^(n1 k2) sum_n2 x[n1 + N1 n2] w_N2^(n2 k2) ],
+// so a thread loads N2 strided inputs straight from HBM into registers, takes an
+// N2-point DFT, applies the twiddles w_N^(n1 k2), writes to LDS; after one barrier a
+// thread gathers N1 values and takes the N1-point DFT.  Channels are on the lanes, so
+// every global access of a wave covers consecutive channels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "afno_internal.h"
+#include "dft_reg.h"
+#include "kernel_common.h"
+
+namespace afno {
+
+// tw[m] = exp(-2 pi i m / N), m in [0, N), from double-precision sincospi (no barrier)
+template <int N, int NT>
+__device__ __forceinline__ void fill_roots(float2* tw) {
+  for (int m = threadIdx.x; m < N; m += NT) {
+    double s, c;
+    sincospi(2.0 * (double)m / (double)N, &s, &c);
+    tw[m] = make_float2((float)c, (float)(-s));
+  }
+}
+
+template <bool INV>
+__device__ __forceinline__ float2 twiddle(float2 v, const float2* tw, int m) {
+  float2 w = tw[m];
+  if (INV) w.y = -w.y;
+  return c_mul(v, w);
+}
+
+// two consecutive elements of T in their storage form, and their widening to float
+template <typename T> struct Raw2;
+template <> struct Raw2<float> { typedef float2 type; };
+template <> struct Raw2<bf16> { typedef uint32_t type; };
+__device__ __forceinline__ float2 ld_raw2(const float* p) { return *reinterpret_cast<const float2*>(p); }
+__device__ __forceinline__ uint32_t ld_raw2(const bf16* p) { return *reinterpret_cast<const uint32_t*>(p); }
+__device__ __forceinline__ float2 widen2(float2 v) { return v; }
+__device__ __forceinline__ float2 widen2(uint32_t v) {
+  return make_float2(__uint_as_float(v << 16), __uint_as_float(v & 0xffff0000u));
+}
+
+// X_c = (Z[k] + conj Z[W-k]) s,  X_{c+1} = (Z[k] - conj Z[W-k]) s / i  with s = 1/(2 sqrt W)
+template <typename T>
+__device__ __forceinline__ void store_split(T* o, float2 z, float2 zm, float s) {
+  st_c2(o, make_float4((z.x + zm.x) * s, (z.y - zm.y) * s, (z.y + zm.y) * s, (zm.x - z.x) * s));
+}
+
+// ------------------------------------------------------------------ W-axis forward
+
+// grid (B * H, C / (2 NP)), block NP * N1.  NP complex signals (2 NP channels) per
+// workgroup; signal p of thread t = t % NP.
+template <typename T, int W, int N1, int N2, int NP>
+__global__ void __launch_bounds__(NP * N1)
+row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float scale) {
+  static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
+  constexpr int NT = NP * N1;
+  __shared__ float2 F[N2 * N1 * NP];
+  __shared__ float2 tw[W];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;  // b * H + h
+  const int c0 = blockIdx.y * (2 * NP);
+  {
+    const int p = tid % NP, j = tid / NP;
+    const T* xr = x + row * (int64_t)W * C + c0 + 2 * p;
+    float2 v[N2];
+#pragma unroll
+    for (int t = 0; t < N2; ++t) v[t] = ld_c(xr + (int64_t)(j + N1 * t) * C);
+    fill_roots<W, NT>(tw);
+    __syncthreads();
+    DftReg<N2, false>::run(v);
+#pragma unroll
+    for (int k2 = 0; k2 < N2; ++k2)
+      F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<false>(v[k2], tw, (j * k2) % W);
+  }
+  __syncthreads();
+  // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
+  // for every k of both residue classes, so the two real spectra separate in registers.
+  constexpr int NPT = N2 / 2 + 1;
+  for (int task = tid; task < NP * NPT; task += NT) {
+    const int p = task % NP, q = task / NP;
+    const int qa = q, qb = (N2 - q) % N2;
+    float2 a[N1], b[N1];
+#pragma unroll
+    for (int j = 0; j < N1; ++j) {
+      a[j] = F[(qa * N1 + j) * NP + p];
+      b[j] = F[(qb * N1 + j) * NP + p];
+    }
+    DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
+    DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
+    T* Sr = S + row * (int64_t)KW * C * 2 + (int64_t)(c0 + 2 * p) * 2;
+#pragma unroll
+    for (int k1 = 0; k1 < N1; ++k1) {
+      // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
+      const int ka = qa + N2 * k1;
+      const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
+      if (ka <= W / 2 && ka < KW) store_split(Sr + (int64_t)ka * C * 2, a[k1], zam, scale);
+      const int kb = qb + N2 * k1;
+      if (qb != qa && kb <= W / 2 && kb < KW)
+        store_split(Sr + (int64_t)kb * C * 2, b[k1], a[N1 - 1 - k1], scale);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ W-axis inverse + residual
+
+// grid (B * H, C / (2 NP)), block NP * N1.  mode 0: out = x + y (dtype T); mode 1: dst = y.
+template <typename T, int W, int N1, int N2, int NP>
+__global__ void __launch_bounds__(NP * N1)
+row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ out,
+             float* __restrict__ dst, int C, int KW, float scale, int mode) {
+  static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
+  constexpr int NT = NP * N1;
+  constexpr int HALF = W / 2;
+  constexpr int TP2 = (NP * N2 + NT - 1) / NT;  // second-stage tasks per thread
+  __shared__ float2 F[N2 * N1 * NP];
+  __shared__ float2 tw[W];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int c0 = blockIdx.y * (2 * NP);
+  // the residual of the second-stage tasks, fetched first so its latency overlaps the
+  // transform (kept in storage form)
+  typename Raw2<T>::type xres[TP2][N1];
+  if (mode == 0) {
+#pragma unroll
+    for (int u = 0; u < TP2; ++u) {
+      const int task = tid + u * NT;
+      if (task < NP * N2) {
+        const int p = task % NP, k2 = task / NP;
+        const T* xr = x + row * (int64_t)W * C + c0 + 2 * p;
+#pragma unroll
+        for (int k1 = 0; k1 < N1; ++k1) xres[u][k1] = ld_raw2(xr + (int64_t)(k2 + N2 * k1) * C);
+      }
+    }
+  }
+  {
+    const int p = tid % NP, j = tid / NP;
+    const T* Sr = S + row * (int64_t)KW * C * 2 + (int64_t)(c0 + 2 * p) * 2;
+    float2 v[N2];
+#pragma unroll
+    for (int t = 0; t < N2; ++t) {
+      // Z[k] = Y_c[k] + i Y_{c+1}[k] over the full length from the stored half:
+      // Y[W - k] = conj Y[k]; only the real parts of the k = 0 and k = W/2 bins count.
+      const int k = j + N1 * t;
+      const int kk = k <= HALF ? k : W - k;
+      float4 y = make_float4(0.f, 0.f, 0.f, 0.f);  // (Re Y_c, Im Y_c, Re Y_c+1, Im Y_c+1)
+      if (kk < KW) y = ld_c2(Sr + (int64_t)kk * C * 2);
+      v[t] = (k == 0 || k == HALF) ? make_float2(y.x, y.z)
+             : (k < HALF ? make_float2(y.x - y.w, y.y + y.z) : make_float2(y.x + y.w, y.z - y.y));
+    }
+    fill_roots<W, NT>(tw);
+    __syncthreads();
+    DftReg<N2, true>::run(v);
+#pragma unroll
+    for (int k2 = 0; k2 < N2; ++k2)
+      F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<true>(v[k2], tw, (j * k2) % W);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < TP2; ++u) {
+    const int task = tid + u * NT;
+    if (task >= NP * N2) break;
+    const int p = task % NP, k2 = task / NP;
+    float2 a[N1];
+#pragma unroll
+    for (int j = 0; j < N1; ++j) a[j] = F[(k2 * N1 + j) * NP + p];
+    DftReg<N1, true>::run(a);  // a[k1] = z[k2 + N2 k1] = y_c + i y_{c+1}
+    const int64_t base = row * (int64_t)W * C + c0 + 2 * p;
+#pragma unroll
+    for (int k1 = 0; k1 < N1; ++k1) {
+      const int64_t off = base + (int64_t)(k2 + N2 * k1) * C;
+      const float2 y = make_float2(a[k1].x * scale, a[k1].y * scale);
+      if (mode == 1) {
+        *reinterpret_cast<float2*>(dst + off) = y;
+      } else {
+        const float2 xv = widen2(xres[u][k1]);
+        st_c(out + off, make_float2(xv.x + y.x, xv.y + y.y));
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ column kernel
+
+template <int BS> struct ColShape {
+  static constexpr int kThreads = 4 * BS < 64 ? 64 : 4 * BS;  // bs / 16 MFMA waves
+};
+
+template <typename T, typename FT, int H, int BS>
+struct ColLds {
+  static constexpr int kH16 = (H + 15) / 16 * 16;
+  static constexpr int kLdt = 2 * BS + (sizeof(T) == 2 ? 8 : 4);
+  static constexpr int kTile = kH16 * kLdt * (int)sizeof(T);
+  static constexpr int kF = H * BS * 2 * (int)sizeof(FT);
+  static constexpr int kRegion = ((kTile > kF ? kTile : kF) + 15) / 16 * 16;
+  static constexpr int kBytes = kRegion + H * 8;
+};
+
+template <typename FT>
+__device__ __forceinline__ void st_f(FT* p, float2 v);
+template <> __device__ __forceinline__ void st_f<float>(float* p, float2 v) { st_c(p, v); }
+template <> __device__ __forceinline__ void st_f<bf16>(bf16* p, float2 v) { st_c(p, v); }
+
+// One layer of the block MLP: acc[m][n] = rows of m-tile m times the real-ified complex
+// weight for the wave's two output tiles n (complex columns jn0, jn1).  Every m-tile is
+// computed (rows outside the cutoff are zeroed by the caller), so the LDS reads of a
+// k-step are issued together.  Weight fragments are fetched at most 8 k-steps at a time.
+template <typename T, int BS, int MT>
+__device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, int jn0, int jn1,
+                                           int sg, f32x4 (&acc)[MT][2]) {
+  typedef Mma<T> M;
+  constexpr int LDT = 2 * BS + (sizeof(T) == 2 ? 8 : 4);
+  constexpr int KSTEPS = 2 * BS / M::kK;
+  constexpr int KCH = KSTEPS < 8 ? KSTEPS : 8;
+  static_assert(KSTEPS % KCH == 0, "k-step chunking");
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[m][0] = acc[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const T* arow = tile + (lane & 15) * LDT;
+#pragma unroll 1
+  for (int s0 = 0; s0 < KSTEPS; s0 += KCH) {
+    typename M::Frag bfr[KCH][2];
+#pragma unroll
+    for (int s = 0; s < KCH; ++s) {
+      bfr[s][0] = M::load_b(w, BS, (s0 + s) * M::kK, jn0, sg, lane);
+      bfr[s][1] = M::load_b(w, BS, (s0 + s) * M::kK, jn1, sg, lane);
+    }
+#pragma unroll
+    for (int s = 0; s < KCH; ++s) {
+      typename M::Frag a[MT];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) a[m] = M::load_a(arow + 16 * m * LDT, (s0 + s) * M::kK, lane);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        acc[m][0] = M::mma(a[m], bfr[s][0], acc[m][0]);
+        acc[m][1] = M::mma(a[m], bfr[s][1], acc[m][1]);
+      }
+    }
+  }
+}
+
+// grid B * KW * nb, block ColShape<BS>::kThreads, dynamic LDS ColLds<...>::kBytes.
+// WPE: waves per SIMD the register budget must allow (the workgroups per CU that the
+// LDS admits times the waves per workgroup, over 4 SIMDs).
+// The transform intermediate (FT: float, or bf16 where float would not fit the LDS)
+// shares its LDS with the MFMA tile; the passes that switch between the two read all
+// of their inputs, synchronise, then write.
+// stage: 0 full, 1 stop after the forward transform, 2 stop after the MLP.
+template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE>
+__global__ void __launch_bounds__(ColShape<BS>::kThreads) __attribute__((amdgpu_waves_per_eu(WPE)))
+column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b1,
+            const T* __restrict__ w2, const T* __restrict__ b2, int C, int KW, int nb,
+            int kept_h, float lam, float scale, int stage) {
+  static_assert(N1 * N2 == H, "H = N1 N2");
+  static_assert(BS % 16 == 0, "block size multiple of 16");
+  typedef ColLds<T, FT, H, BS> L;
+  constexpr int NT = ColShape<BS>::kThreads;
+  constexpr int MT = L::kH16 / 16;
+  constexpr int LDT = L::kLdt;
+  extern __shared__ float4 smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);
+  FT* F = reinterpret_cast<FT*>(smem_raw);
+  float2* tw = reinterpret_cast<float2*>(reinterpret_cast<char*>(smem_raw) + L::kRegion);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  const int blk = blockIdx.x % nb;  // consecutive workgroups -> different XCDs -> blocks
+  const int rest = blockIdx.x / nb;
+  const int kw = rest % KW;
+  const int64_t b = rest / KW;
+  const int64_t rs = (int64_t)KW * C * 2;  // row stride of S, elements
+  T* col = S + ((b * H) * KW + kw) * (int64_t)C * 2 + (int64_t)blk * BS * 2;
+
+  // ---- forward, first stage: task (c, j): rows j + N1 t of channel c from HBM
+  constexpr int TA = (BS * N1 + NT - 1) / NT;
+  {
+    float2 va[TA][N2];
+#pragma unroll
+    for (int u = 0; u < TA; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N1) {
+        const int c = task % BS, j = task / BS;
+#pragma unroll
+        for (int t = 0; t < N2; ++t) va[u][t] = ld_c(col + (int64_t)(j + N1 * t) * rs + 2 * c);
+      }
+    }
+    fill_roots<H, NT>(tw);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < TA; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N1) {
+        const int c = task % BS, j = task / BS;
+        DftReg<N2, false>::run(va[u]);
+#pragma unroll
+        for (int k2 = 0; k2 < N2; ++k2)
+          st_f(F + ((k2 * N1 + j) * BS + c) * 2,
+               k2 == 0 ? va[u][0] : twiddle<false>(va[u][k2], tw, (j * k2) % H));
+      }
+    }
+  }
+  __syncthreads();
+  // ---- forward, second stage: task (c, k2) -> spectrum rows k2 + N2 k1 into the tile
+  constexpr int TB = (BS * N2 + NT - 1) / NT;
+  {
+    float2 vb[TB][N1];
+#pragma unroll
+    for (int u = 0; u < TB; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N2) {
+        const int c = task % BS, k2 = task / BS;
+#pragma unroll
+        for (int j = 0; j < N1; ++j) vb[u][j] = ld_c(F + ((k2 * N1 + j) * BS + c) * 2);
+      }
+    }
+    __syncthreads();  // the tile overwrites F
+#pragma unroll
+    for (int u = 0; u < TB; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N2) {
+        const int c = task % BS, k2 = task / BS;
+        DftReg<N1, false>::run(vb[u]);
+#pragma unroll
+        for (int k1 = 0; k1 < N1; ++k1)
+          st_c(tile + (k2 + N2 * k1) * LDT + 2 * c,
+               make_float2(vb[u][k1].x * scale, vb[u][k1].y * scale));
+      }
+    }
+    for (int e = tid; e < (L::kH16 - H) * 2 * BS; e += NT)
+      tile[(H + e / (2 * BS)) * LDT + e % (2 * BS)] = Store<T>::to(0.f);
+  }
+  __syncthreads();
+
+  if (stage != 1) {
+    // ---- block MLP: wave w owns real output columns [32 w, 32 w + 32) (16 complex)
+    const int nu0 = 32 * wave + (lane & 15);
+    const int jn0 = nu0 >> 1, jn1 = jn0 + 8, sg = lane & 1;
+    const T* W1 = w1 + (int64_t)blk * BS * BS * 2;
+    const T* W2 = w2 + (int64_t)blk * BS * BS * 2;
+    const T* B1 = b1 + (int64_t)blk * BS * 2;
+    const T* B2 = b2 + (int64_t)blk * BS * 2;
+    f32x4 acc[MT][2];
+    // layer 1
+    gemm_layer<T, BS, MT>(tile, W1, lane, jn0, jn1, sg, acc);
+    const float bias10 = ld_f(B1 + nu0), bias11 = ld_f(B1 + nu0 + 16);
+    const float bias20 = ld_f(B2 + nu0), bias21 = ld_f(B2 + nu0 + 16);
+    __syncthreads();  // every wave has read the spectrum rows
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        tile[row * LDT + nu0] = Store<T>::to(fmaxf(acc[m][0][r] + bias10, 0.f));
+        tile[row * LDT + nu0 + 16] = Store<T>::to(fmaxf(acc[m][1][r] + bias11, 0.f));
+      }
+    }
+    __syncthreads();  // hidden layer complete
+    gemm_layer<T, BS, MT>(tile, W2, lane, jn0, jn1, sg, acc);
+    __syncthreads();  // every wave has read the hidden rows
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        const bool keep = row_kept(row, H, kept_h);
+        const float o0 = softshrink(acc[m][0][r] + bias20, lam);
+        const float o1 = softshrink(acc[m][1][r] + bias21, lam);
+        tile[row * LDT + nu0] = Store<T>::to(keep ? o0 : 0.f);
+        tile[row * LDT + nu0 + 16] = Store<T>::to(keep ? o1 : 0.f);
+      }
+    }
+    __syncthreads();
+  }
+
+  if (stage != 0) {  // diagnostic stop: the tile goes back to S as it is
+    constexpr int V = Store<T>::kVec;
+    constexpr int VPR = 2 * BS / V;
+    for (int it = tid; it < H * VPR; it += NT) {
+      const int h = it / VPR, cv = it - h * VPR;
+      *reinterpret_cast<uint4*>(col + h * rs + cv * V) =
+          *reinterpret_cast<const uint4*>(tile + h * LDT + cv * V);
+    }
+    return;
+  }
+
+  // ---- inverse, first stage: task (c, j): tile rows j + N1 t
+  constexpr int TC = (BS * N1 + NT - 1) / NT;
+  {
+    float2 vc[TC][N2];
+#pragma unroll
+    for (int u = 0; u < TC; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N1) {
+        const int c = task % BS, j = task / BS;
+#pragma unroll
+        for (int t = 0; t < N2; ++t) vc[u][t] = ld_c(tile + (j + N1 * t) * LDT + 2 * c);
+      }
+    }
+    __syncthreads();  // F overwrites the tile
+#pragma unroll
+    for (int u = 0; u < TC; ++u) {
+      const int task = tid + u * NT;
+      if (task < BS * N1) {
+        const int c = task % BS, j = task / BS;
+        DftReg<N2, true>::run(vc[u]);
+#pragma unroll
+        for (int k2 = 0; k2 < N2; ++k2)
+          st_f(F + ((k2 * N1 + j) * BS + c) * 2,
+               k2 == 0 ? vc[u][0] : twiddle<true>(vc[u][k2], tw, (j * k2) % H));
+      }
+    }
+  }
+  __syncthreads();
+  // ---- inverse, second stage: task (c, k2) -> rows k2 + N2 k1 of S
+  for (int task = tid; task < BS * N2; task += NT) {
+    const int c = task % BS, k2 = task / BS;
+    float2 vd[N1];
+#pragma unroll
+    for (int j = 0; j < N1; ++j) vd[j] = ld_c(F + ((k2 * N1 + j) * BS + c) * 2);
+    DftReg<N1, true>::run(vd);
+#pragma unroll
+    for (int k1 = 0; k1 < N1; ++k1)
+      st_c(col + (int64_t)(k2 + N2 * k1) * rs + 2 * c,
+           make_float2(vd[k1].x * scale, vd[k1].y * scale));
+  }
+}
+
+}  // namespace afno

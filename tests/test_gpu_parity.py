@@ -27,6 +27,19 @@ def _need_gpu():
     afno.load_library()
 
 
+_PATH = {"now": "auto"}
+
+
+@pytest.fixture(params=["auto", "generic"])
+def kernel_path(request):
+    """Run a test on the size-specialised kernels (auto) and on the size-generic ones."""
+    afno.set_kernel_path(afno.AFNO_PATH_GENERIC if request.param == "generic" else afno.AFNO_PATH_AUTO)
+    _PATH["now"] = request.param
+    yield request.param
+    afno.set_kernel_path(afno.AFNO_PATH_AUTO)
+    _PATH["now"] = "auto"
+
+
 def _run(x_st, w_st, wl, stage=None, keep=None):
     x = to_dev(x_st, wl.dtype)
     w = dev_weights(w_st, wl.dtype)
@@ -42,7 +55,7 @@ def _run(x_st, w_st, wl, stage=None, keep=None):
 
 def _check_full(wl, x_st, w_st, label):
     say(f"[parity] {label}: B={x_st.shape[0]} H={wl.H} W={wl.W} C={wl.C} nb={wl.num_blocks} "
-        f"{wl.dtype} keep={wl.keep}")
+        f"{wl.dtype} keep={wl.keep} path={_PATH['now']}")
     g = _run(x_st, w_st, wl)
     r, st = oracle_run(x_st, w_st, wl, stages=True)
     x64 = synth.widen(x_st, wl.dtype)
@@ -62,22 +75,22 @@ def _check_full(wl, x_st, w_st, label):
 # ---------------------------------------------------------------- the five workloads
 
 
-def test_afno16x32_fp32_full():
+def test_afno16x32_fp32_full(kernel_path):
     wl = synth.WORKLOADS["afno16x32_c64_nb4_fp32"]
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
-def test_afno90x180_fp32_full():
+def test_afno90x180_fp32_full(kernel_path):
     wl = synth.WORKLOADS["afno90x180_c768_nb8_fp32"]
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
-def test_afno90x180_bf16_b4_full():
+def test_afno90x180_bf16_b4_full(kernel_path):
     wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"]
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
-def test_afno180x360_bf16_sampled_blocks():
+def test_afno180x360_bf16_sampled_blocks(kernel_path):
     """Full 1 x 180 x 360 x 1024 call; the oracle recomputes blocks 0 and 7 alone."""
     wl = synth.WORKLOADS["afno180x360_c1024_nb8_bf16"]
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
@@ -96,7 +109,7 @@ def test_afno180x360_bf16_sampled_blocks():
         assert e_out <= TOL["bf16"] and e_delta <= TOL["bf16"]
 
 
-def test_afno90x180_bf16_ensemble100_keep05_sampled_members():
+def test_afno90x180_bf16_ensemble100_keep05_sampled_members(kernel_path):
     """Full 100-member call with keep 0.5; the oracle recomputes members 0, 57 and 99."""
     wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
     say(f"[parity] {wl.name}: generating 100 members")
@@ -116,7 +129,7 @@ def test_afno90x180_bf16_ensemble100_keep05_sampled_members():
 
 
 @pytest.mark.parametrize("name", ["afno16x32_c64_nb4_fp32", "afno90x180_c768_nb8_fp32"])
-def test_stage_spectra_fp32(name):
+def test_stage_spectra_fp32(name, kernel_path):
     wl = synth.WORKLOADS[name]
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
     say(f"[stage] {name}")
@@ -129,7 +142,7 @@ def test_stage_spectra_fp32(name):
     assert e1 <= 1e-5 and e2 <= 1e-4
 
 
-def test_stage_spectra_bf16():
+def test_stage_spectra_bf16(kernel_path):
     wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"]
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
     x_st = x_st[:1]
@@ -160,6 +173,11 @@ EDGE = [
     (1, 45, 360, 64, 4, "bf16", 0.01, 1.0),
     (2, 18, 24, 64, 1, "fp32", 0.005, 1.0),
     (1, 81, 12, 80, 5, "fp32", 0.01, 0.9),
+    # grids with size-specialised W kernels but generic column kernels, and the reverse
+    (2, 30, 180, 64, 2, "bf16", 0.01, 1.0),
+    (1, 90, 32, 192, 2, "fp32", 0.01, 0.8),
+    (1, 16, 360, 96, 1, "bf16", 0.01, 0.5),
+    (3, 16, 40, 64, 4, "bf16", 0.01, 1.0),
 ]
 
 
@@ -179,7 +197,7 @@ def _zero_weights(wl):
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_zero_weights_bit_exact_identity(dtype):
+def test_zero_weights_bit_exact_identity(dtype, kernel_path):
     wl = synth.Workload("zero", 2, 90, 180, 128, 2, dtype, 0.0, 1.0)
     say(f"[edge] zero weights {dtype}")
     x_st = synth.make_x(wl)
@@ -188,7 +206,7 @@ def test_zero_weights_bit_exact_identity(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_nothing_kept_bit_exact_identity(dtype):
+def test_nothing_kept_bit_exact_identity(dtype, kernel_path):
     wl = synth.Workload("cut", 2, 16, 32, 64, 4, dtype, 0.01, 0.05)
     say(f"[edge] nothing kept {dtype}")
     x_st = synth.make_x(wl)
@@ -196,7 +214,7 @@ def test_nothing_kept_bit_exact_identity(dtype):
     assert np.array_equal(g, synth.widen(x_st, dtype))
 
 
-def test_dc_only_cutoff():
+def test_dc_only_cutoff(kernel_path):
     wl = synth.Workload("dc", 2, 16, 32, 64, 4, "fp32", 0.01, 0.115)
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), "DC-only cutoff")
 
@@ -208,7 +226,7 @@ def test_batch_zero_is_noop():
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_deterministic_bitwise(dtype):
+def test_deterministic_bitwise(dtype, kernel_path):
     wl = synth.Workload("det", 2, 90, 180, 192, 2, dtype, 0.01, 1.0)
     say(f"[edge] determinism {dtype}")
     x = to_dev(synth.make_x(wl), dtype)
