@@ -32,6 +32,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3       # fp32 matrix
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_afno90x180_c768_nb8_bf16_b4.json")
+# HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
+# sha256 of the kernel sources it was measured on (null once the kernels change)
 
 
 def kernel_source_hash() -> str:
@@ -136,22 +138,43 @@ def roofline(wl, kern_ms: dict, es: int):
     return roof, per
 
 
-def cpu_baseline(wl, n_samples: int):
-    import numpy as np
-
+def cpu_baseline(wl, min_seconds: float):
+    """The float64 oracle on the workload's samples, one sample per call, repeated until
+    at least min_seconds of wall time have passed."""
     import oracle
     from paper_2208_05419_amd import synth
 
-    x = synth.widen(synth.make_x(wl, members=list(range(n_samples))), wl.dtype)
+    x = synth.widen(synth.make_x(wl), wl.dtype)
     w = {k: synth.widen(v, wl.dtype) for k, v in synth.make_weights(wl).items()}
+    done = 0
     t0 = time.perf_counter()
-    oracle.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep)
-    dt = time.perf_counter() - t0
-    del np
-    return {"value": round(n_samples / dt, 4), "unit": "samples/s", "cores": oracle.num_threads(),
+    while True:
+        b = done % wl.B
+        oracle.filter_forward(x[b:b + 1], w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks,
+                              wl.lam, wl.keep)
+        done += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": round(done / dt, 4), "unit": "samples/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"{n_samples} of the {wl.B} samples of {wl.name} (float64 direct DFT, "
-                      f"{dt:.1f} s wall)"}
+            "sample": f"{done} single-sample calls cycling over the {wl.B} samples of {wl.name} "
+                      f"(float64 direct DFT, {dt:.1f} s wall)"}
+
+
+def calibration_copy(mib: int):
+    """One device-to-device copy of exactly mib MiB (a plain copy kernel of known size that
+    hardware-counter runs use to scale FETCH_SIZE and WRITE_SIZE)."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def main():
@@ -161,7 +184,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-ensemble", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=2)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
+                    help="run one plain copy of this many MiB first (for counter scaling)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -176,6 +201,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     afno.load_library()
+    if args.calibrate_copy:
+        calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[synth.HEADLINE]
     es = 2 if wl.dtype == "bf16" else 4
     ms, kern_ms, calls = time_workload(wl, args.steps, args.warmup)
@@ -208,7 +235,7 @@ def main():
         line["ensemble"] = {"workload": ens.name, "samples_per_s": round(ens.B / (e_ms * 1e-3), 2),
                             "ms_per_step": round(e_ms, 4), "kernels": e_per, "roofline": e_roof}
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_samples)
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
 
 
