@@ -76,12 +76,13 @@ static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, 
 #undef AFNO_CASE
 }
 
-template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE>
+template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE,
+          int NT = ColShape<BS>::kThreads>
 static void launch_col_fast_one(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
                                 const T* b2, int stage, hipStream_t st) {
   constexpr int lds = ColLds<T, FT, H, BS>::kBytes;
-  constexpr int nthr = ColShape<BS>::kThreads;
-  hipLaunchKernelGGL((column_fast<T, FT, H, N1, N2, BS, WPE>), dim3((unsigned)(pl.B * pl.KW * pl.nb)),
+  constexpr int nthr = NT;
+  hipLaunchKernelGGL((column_fast<T, FT, H, N1, N2, BS, WPE, NT>), dim3((unsigned)(pl.B * pl.KW * pl.nb)),
                      dim3(nthr), lds, st, S, w1, b1, w2, b2, (int)pl.C, (int)pl.KW, (int)pl.nb,
                      (int)pl.kept_h, pl.col.lam, pl.col.inv_sqrt_h, stage);
 }
@@ -92,7 +93,7 @@ static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, cons
   if (pl.H == 16 && pl.bs == 16)
     launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, w1, b1, w2, b2, stage, st);
   else if (pl.H == 90 && pl.bs == 96)
-    launch_col_fast_one<T, float, 90, 9, 10, 96, 3>(pl, S, w1, b1, w2, b2, stage, st);
+    launch_col_fast_one<T, float, 90, 9, 10, 96, 4, 512>(pl, S, w1, b1, w2, b2, stage, st);
   else if constexpr (sizeof(T) == 2)
     launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, w1, b1, w2, b2, stage, st);
 }
@@ -164,11 +165,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(row_c2r_kernel<bf16>)
   AFNO_ATTR(column_kernel<float>)
   AFNO_ATTR(column_kernel<bf16>)
-  AFNO_ATTR((column_fast<float, float, 16, 4, 4, 16, 4>))
-  AFNO_ATTR((column_fast<bf16, float, 16, 4, 4, 16, 4>))
-  AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 3>))
-  AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 3>))
-  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2>))
+  AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
+  AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
+  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))
 #undef AFNO_ATTR
   return first;
 }

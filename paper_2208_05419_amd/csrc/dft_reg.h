@@ -2,11 +2,14 @@
 //
 // DftReg<N, INV>::run(v) replaces v[0..N) by X[k] = sum_n v[n] exp(-+2 pi i n k / N)
 // (INV: exp(+...)), unscaled, natural order in and out.  N is a compile-time product
-// of 2, 3, 4 and 5.  A composite N = P * M is split by one decimation-in-time step
-// (Cooley and Tukey): the P interleaved subsequences v[r + P m] get M-point DFTs U_r,
-// U_r[k] is multiplied by exp(-+2 pi i r k / N), and for each k a P-point DFT over r
-// gives X[k + M q], q in [0, P).  All indices are compile-time constants after
-// unrolling, so the values stay in VGPRs.
+// of 2, 3, 4 and 5.  A composite N = P * M is split in one of two ways:
+//  * gcd(P, M) = 1: the prime-factor algorithm (Good; Thomas): with n = (M p + P m) mod N
+//    and k = (M a kp + P b km) mod N, a = M^-1 mod P, b = P^-1 mod M, the DFT is an
+//    M-point DFT along m followed by a P-point DFT along p with no twiddle factors;
+//  * otherwise one decimation-in-time step (Cooley and Tukey): the P interleaved
+//    subsequences v[r + P m] get M-point DFTs U_r, U_r[k] is multiplied by
+//    exp(-+2 pi i r k / N), and for each k a P-point DFT over r gives X[k + M q].
+// All indices are compile-time constants after unrolling, so the values stay in VGPRs.
 //
 // The twiddle constants are evaluated at compile time from Taylor series of sin and
 // cos on the first quadrant (terms to x^29, far below double rounding there), with
@@ -65,6 +68,23 @@ struct Roots {
 
 constexpr int first_factor(int n) {
   return (n % 4 == 0 && n != 4) ? 4 : (n % 2 == 0 ? 2 : (n % 3 == 0 ? 3 : 5));
+}
+
+constexpr int gcd(int a, int b) { return b == 0 ? a : gcd(b, a % b); }
+
+// the full power of the smallest prime dividing n (n itself when n is a prime power)
+constexpr int prime_power(int n) {
+  const int p = n % 2 == 0 ? 2 : (n % 3 == 0 ? 3 : 5);
+  int q = 1;
+  while (n % (q * p) == 0) q *= p;
+  return q;
+}
+
+// x^-1 mod m for gcd(x, m) = 1
+constexpr int inv_mod(int x, int m) {
+  for (int y = 1; y < m; ++y)
+    if ((x * y) % m == 1) return y;
+  return m == 1 ? 0 : -1;
 }
 
 }  // namespace ct
@@ -131,11 +151,31 @@ __host__ __device__ __forceinline__ float2 root(int m) {
 
 template <int N, bool INV>
 struct DftReg {
-  static constexpr int P = (N <= 5 || N == 4) ? N : ct::first_factor(N);
+  // coprime split where N has two distinct primes, else a radix-4/2/3/5 step
+  static constexpr bool kPfa = N > 5 && ct::prime_power(N) != N;
+  static constexpr int P = (N <= 5) ? N : (kPfa ? ct::prime_power(N) : ct::first_factor(N));
   static constexpr int M = N / P;
   __host__ __device__ __forceinline__ static void run(float2* v) {
     if constexpr (M == 1) {
       butterfly<P, INV>(v);
+    } else if constexpr (kPfa) {
+      constexpr int A = ct::inv_mod(M % P, P), Bm = ct::inv_mod(P % M, M);
+      float2 u[P][M];
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+#pragma unroll
+        for (int m = 0; m < M; ++m) u[p][m] = v[(M * p + P * m) % N];
+#pragma unroll
+      for (int p = 0; p < P; ++p) DftReg<M, INV>::run(u[p]);
+#pragma unroll
+      for (int km = 0; km < M; ++km) {
+        float2 w[P];
+#pragma unroll
+        for (int p = 0; p < P; ++p) w[p] = u[p][km];
+        DftReg<P, INV>::run(w);
+#pragma unroll
+        for (int kp = 0; kp < P; ++kp) v[(M * A * kp + P * Bm * km) % N] = w[kp];
+      }
     } else {
       float2 u[P][M];
 #pragma unroll

@@ -122,8 +122,39 @@ __device__ __forceinline__ bool row_kept(int r, int H, int kept_h) {
   return s < kept_h;
 }
 
+// S(v) = v - lam (v > lam), v + lam (v < -lam), else 0, written as v - clamp(v, -lam, lam)
+// (exactly 0 inside the band, exact shifts outside it)
 __device__ __forceinline__ float softshrink(float v, float lam) {
-  return v > lam ? v - lam : (v < -lam ? v + lam : 0.f);
+  return v - __builtin_amdgcn_fmed3f(v, -lam, lam);
+}
+
+// Raw buffer access: a per-workgroup base in a scalar resource descriptor, a 32-bit
+// per-lane byte offset and a wave-uniform byte offset, so addressing costs no 64-bit
+// vector arithmetic.  Accesses beyond `bytes` read 0 and do not write.
+struct Buf {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ __forceinline__ Buf(const void* base, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                            0x00020000)) {}
+  __device__ __forceinline__ uint32_t ld32(uint32_t voff, uint32_t soff) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+  }
+  __device__ __forceinline__ void st32(uint32_t v, uint32_t voff, uint32_t soff) const {
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
+  }
+};
+__device__ __forceinline__ uint32_t buf_bytes(uint64_t n) {
+  return n >= 0xffffffffull ? 0xffffffffu : (uint32_t)n;
+}
+// one complex value from / to 32 bits of storage
+__device__ __forceinline__ float2 unpack_c(uint32_t v, const bf16*) {
+  return make_float2(__uint_as_float(v << 16), __uint_as_float(v & 0xffff0000u));
+}
+__device__ __forceinline__ uint32_t pack_c(float2 z, const bf16*) {
+  union { uint32_t u; bf16 h[2]; } w;
+  w.h[0] = (bf16)z.x;
+  w.h[1] = (bf16)z.y;
+  return w.u;
 }
 
 }  // namespace afno

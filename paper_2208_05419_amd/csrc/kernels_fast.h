@@ -47,6 +47,32 @@ __device__ __forceinline__ float2 widen2(uint32_t v) {
   return make_float2(__uint_as_float(v << 16), __uint_as_float(v & 0xffff0000u));
 }
 
+// complex values of storage type T through a buffer descriptor (byte offsets)
+template <typename T> struct CBuf;
+template <> struct CBuf<bf16> {
+  Buf b;
+  __device__ __forceinline__ CBuf(const bf16* base, uint32_t bytes) : b(base, bytes) {}
+  __device__ __forceinline__ float2 ld(uint32_t voff, uint32_t soff) const {
+    return unpack_c(b.ld32(voff, soff), (const bf16*)nullptr);
+  }
+  __device__ __forceinline__ void st(uint32_t voff, uint32_t soff, float2 z) const {
+    b.st32(pack_c(z, (const bf16*)nullptr), voff, soff);
+  }
+};
+template <> struct CBuf<float> {
+  Buf b;
+  __device__ __forceinline__ CBuf(const float* base, uint32_t bytes) : b(base, bytes) {}
+  __device__ __forceinline__ float2 ld(uint32_t voff, uint32_t soff) const {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(b.r, voff, soff, 0);
+    return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+  }
+  __device__ __forceinline__ void st(uint32_t voff, uint32_t soff, float2 z) const {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    u2 v = {__float_as_uint(z.x), __float_as_uint(z.y)};
+    __builtin_amdgcn_raw_buffer_store_b64(v, b.r, voff, soff, 0);
+  }
+};
+
 // X_c = (Z[k] + conj Z[W-k]) s,  X_{c+1} = (Z[k] - conj Z[W-k]) s / i  with s = 1/(2 sqrt W)
 template <typename T>
 __device__ __forceinline__ void store_split(T* o, float2 z, float2 zm, float s) {
@@ -208,59 +234,78 @@ __device__ __forceinline__ void st_f(FT* p, float2 v);
 template <> __device__ __forceinline__ void st_f<float>(float* p, float2 v) { st_c(p, v); }
 template <> __device__ __forceinline__ void st_f<bf16>(bf16* p, float2 v) { st_c(p, v); }
 
-// One layer of the block MLP: acc[m][n] = rows of m-tile m times the real-ified complex
-// weight for the wave's two output tiles n (complex columns jn0, jn1).  Every m-tile is
-// computed (rows outside the cutoff are zeroed by the caller), so the LDS reads of a
-// k-step are issued together.  Weight fragments are fetched at most 8 k-steps at a time.
-template <typename T, int BS, int MT>
-__device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, int jn0, int jn1,
-                                           int sg, f32x4 (&acc)[MT][2]) {
+// Wave grid of the block MLP: WM row groups x WN column groups.  Wave (wm, wn) computes
+// MW = MT / WM m-tiles (rows 16 MW wm ...) by NW = (2 BS / 16) / WN n-tiles (real output
+// columns 16 NW wn ...).  Two row groups halve the LDS traffic of the A tile (each wave
+// reads only its rows) against re-reading each weight column from L2 twice.
+template <int NT, int BS, int MT>
+struct MlpGrid {
+  static constexpr int kWaves = NT / 64;
+  static constexpr int WM = (kWaves >= 4 && MT % 2 == 0) ? 2 : 1;
+  static constexpr int WN = kWaves / WM;
+  static constexpr int MW = MT / WM;
+  static constexpr int NW = (2 * BS / 16) / WN;
+  static_assert(WM * WN == kWaves && MW * WM == MT && NW * WN * 16 == 2 * BS, "MLP wave grid");
+};
+
+// One layer: acc[m][n] = (rows of the wave's m-tile m) x (real-ified complex weight of its
+// n-tile n).  Every m-tile is computed (rows outside the cutoff are zeroed by the caller).
+// Weight fragments are fetched KCH k-steps at a time (a byte permutation per dword turns a
+// complex weight into the two real columns it feeds).
+template <typename T, int NT, int BS, int MT>
+__device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, int wm, int wn,
+                                           f32x4 (&acc)[MlpGrid<NT, BS, MT>::MW][MlpGrid<NT, BS, MT>::NW]) {
   typedef Mma<T> M;
+  typedef MlpGrid<NT, BS, MT> G;
   constexpr int LDT = 2 * BS + (sizeof(T) == 2 ? 8 : 4);
   constexpr int KSTEPS = 2 * BS / M::kK;
-  constexpr int KCH = KSTEPS < 8 ? KSTEPS : 8;
+  constexpr int KCH0 = sizeof(T) == 2 ? 2 : 4;
+  constexpr int KCH = KSTEPS < KCH0 ? KSTEPS : KCH0;
   static_assert(KSTEPS % KCH == 0, "k-step chunking");
+  const int sg = lane & 1;
+  int jn[G::NW];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m][0] = acc[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const T* arow = tile + (lane & 15) * LDT;
+  for (int n = 0; n < G::NW; ++n) jn[n] = (16 * (wn * G::NW + n) + (lane & 15)) >> 1;
+#pragma unroll
+  for (int m = 0; m < G::MW; ++m)
+#pragma unroll
+    for (int n = 0; n < G::NW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const T* arow = tile + (16 * G::MW * wm + (lane & 15)) * LDT;
 #pragma unroll 1
   for (int s0 = 0; s0 < KSTEPS; s0 += KCH) {
-    typename M::Frag bfr[KCH][2];
+    typename M::Frag bfr[KCH][G::NW];
+#pragma unroll
+    for (int s = 0; s < KCH; ++s)
+#pragma unroll
+      for (int n = 0; n < G::NW; ++n) bfr[s][n] = M::load_b(w, BS, (s0 + s) * M::kK, jn[n], sg, lane);
 #pragma unroll
     for (int s = 0; s < KCH; ++s) {
-      bfr[s][0] = M::load_b(w, BS, (s0 + s) * M::kK, jn0, sg, lane);
-      bfr[s][1] = M::load_b(w, BS, (s0 + s) * M::kK, jn1, sg, lane);
-    }
+      typename M::Frag a[G::MW];
 #pragma unroll
-    for (int s = 0; s < KCH; ++s) {
-      typename M::Frag a[MT];
+      for (int m = 0; m < G::MW; ++m) a[m] = M::load_a(arow + 16 * m * LDT, (s0 + s) * M::kK, lane);
 #pragma unroll
-      for (int m = 0; m < MT; ++m) a[m] = M::load_a(arow + 16 * m * LDT, (s0 + s) * M::kK, lane);
+      for (int m = 0; m < G::MW; ++m)
 #pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        acc[m][0] = M::mma(a[m], bfr[s][0], acc[m][0]);
-        acc[m][1] = M::mma(a[m], bfr[s][1], acc[m][1]);
-      }
+        for (int n = 0; n < G::NW; ++n) acc[m][n] = M::mma(a[m], bfr[s][n], acc[m][n]);
     }
   }
 }
 
-// grid B * KW * nb, block ColShape<BS>::kThreads, dynamic LDS ColLds<...>::kBytes.
+// grid B * KW * nb, block NT threads, dynamic LDS ColLds<...>::kBytes.
 // WPE: waves per SIMD the register budget must allow (the workgroups per CU that the
 // LDS admits times the waves per workgroup, over 4 SIMDs).
 // The transform intermediate (FT: float, or bf16 where float would not fit the LDS)
 // shares its LDS with the MFMA tile; the passes that switch between the two read all
 // of their inputs, synchronise, then write.
 // stage: 0 full, 1 stop after the forward transform, 2 stop after the MLP.
-template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE>
-__global__ void __launch_bounds__(ColShape<BS>::kThreads) __attribute__((amdgpu_waves_per_eu(WPE)))
+template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE, int NT>
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE)))
 column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b1,
             const T* __restrict__ w2, const T* __restrict__ b2, int C, int KW, int nb,
             int kept_h, float lam, float scale, int stage) {
   static_assert(N1 * N2 == H, "H = N1 N2");
   static_assert(BS % 16 == 0, "block size multiple of 16");
   typedef ColLds<T, FT, H, BS> L;
-  constexpr int NT = ColShape<BS>::kThreads;
   constexpr int MT = L::kH16 / 16;
   constexpr int LDT = L::kLdt;
   extern __shared__ float4 smem_raw[];
@@ -275,6 +320,8 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
   const int64_t b = rest / KW;
   const int64_t rs = (int64_t)KW * C * 2;  // row stride of S, elements
   T* col = S + ((b * H) * KW + kw) * (int64_t)C * 2 + (int64_t)blk * BS * 2;
+  const uint32_t rsb = (uint32_t)(rs * sizeof(T));  // row stride of S, bytes
+  const CBuf<T> cb(col, buf_bytes((uint64_t)H * rsb));
 
   // ---- forward, first stage: task (c, j): rows j + N1 t of channel c from HBM
   constexpr int TA = (BS * N1 + NT - 1) / NT;
@@ -286,7 +333,8 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
       if (task < BS * N1) {
         const int c = task % BS, j = task / BS;
 #pragma unroll
-        for (int t = 0; t < N2; ++t) va[u][t] = ld_c(col + (int64_t)(j + N1 * t) * rs + 2 * c);
+        for (int t = 0; t < N2; ++t)
+          va[u][t] = cb.ld(2 * c * (uint32_t)sizeof(T) + j * rsb, N1 * t * rsb);
       }
     }
     fill_roots<H, NT>(tw);
@@ -337,41 +385,46 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
   __syncthreads();
 
   if (stage != 1) {
-    // ---- block MLP: wave w owns real output columns [32 w, 32 w + 32) (16 complex)
-    const int nu0 = 32 * wave + (lane & 15);
-    const int jn0 = nu0 >> 1, jn1 = jn0 + 8, sg = lane & 1;
+    // ---- block MLP on the wave grid
+    typedef MlpGrid<NT, BS, MT> G;
+    const int wm = wave / G::WN, wn = wave % G::WN;
     const T* W1 = w1 + (int64_t)blk * BS * BS * 2;
     const T* W2 = w2 + (int64_t)blk * BS * BS * 2;
     const T* B1 = b1 + (int64_t)blk * BS * 2;
     const T* B2 = b2 + (int64_t)blk * BS * 2;
-    f32x4 acc[MT][2];
-    // layer 1
-    gemm_layer<T, BS, MT>(tile, W1, lane, jn0, jn1, sg, acc);
-    const float bias10 = ld_f(B1 + nu0), bias11 = ld_f(B1 + nu0 + 16);
-    const float bias20 = ld_f(B2 + nu0), bias21 = ld_f(B2 + nu0 + 16);
-    __syncthreads();  // every wave has read the spectrum rows
+    const int col0 = 16 * G::NW * wn + (lane & 15);  // real output column of n-tile 0
+    const int row0 = 16 * G::MW * wm + 4 * (lane >> 4);
+    const bool all_rows = kept_h > H / 2;  // cutoff keeps every row
+    f32x4 acc[G::MW][G::NW];
+    gemm_layer<T, NT, BS, MT>(tile, W1, lane, wm, wn, acc);
+    float bias[G::NW];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
+    for (int n = 0; n < G::NW; ++n) bias[n] = ld_f(B1 + col0 + 16 * n);
+    __syncthreads();  // every wave has read its spectrum rows
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * m + 4 * (lane >> 4) + r;
-        tile[row * LDT + nu0] = Store<T>::to(fmaxf(acc[m][0][r] + bias10, 0.f));
-        tile[row * LDT + nu0 + 16] = Store<T>::to(fmaxf(acc[m][1][r] + bias11, 0.f));
-      }
-    }
+    for (int m = 0; m < G::MW; ++m)
+#pragma unroll
+      for (int n = 0; n < G::NW; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          tile[(row0 + 16 * m + r) * LDT + col0 + 16 * n] =
+              Store<T>::to(fmaxf(acc[m][n][r] + bias[n], 0.f));
     __syncthreads();  // hidden layer complete
-    gemm_layer<T, BS, MT>(tile, W2, lane, jn0, jn1, sg, acc);
-    __syncthreads();  // every wave has read the hidden rows
+    gemm_layer<T, NT, BS, MT>(tile, W2, lane, wm, wn, acc);
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
+    for (int n = 0; n < G::NW; ++n) bias[n] = ld_f(B2 + col0 + 16 * n);
+    __syncthreads();  // every wave has read its hidden rows
+#pragma unroll
+    for (int m = 0; m < G::MW; ++m) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = 16 * m + 4 * (lane >> 4) + r;
-        const bool keep = row_kept(row, H, kept_h);
-        const float o0 = softshrink(acc[m][0][r] + bias20, lam);
-        const float o1 = softshrink(acc[m][1][r] + bias21, lam);
-        tile[row * LDT + nu0] = Store<T>::to(keep ? o0 : 0.f);
-        tile[row * LDT + nu0 + 16] = Store<T>::to(keep ? o1 : 0.f);
+        const int row = row0 + 16 * m + r;
+        const bool keep = all_rows || row_kept(row, H, kept_h);
+#pragma unroll
+        for (int n = 0; n < G::NW; ++n) {
+          const float o = softshrink(acc[m][n][r] + bias[n], lam);
+          tile[row * LDT + col0 + 16 * n] = Store<T>::to(keep ? o : 0.f);
+        }
       }
     }
     __syncthreads();
@@ -425,7 +478,7 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
     DftReg<N1, true>::run(vd);
 #pragma unroll
     for (int k1 = 0; k1 < N1; ++k1)
-      st_c(col + (int64_t)(k2 + N2 * k1) * rs + 2 * c,
+      cb.st(2 * c * (uint32_t)sizeof(T) + k2 * rsb, N2 * k1 * rsb,
            make_float2(vd[k1].x * scale, vd[k1].y * scale));
   }
 }
