@@ -140,6 +140,8 @@ int make_plan(const Args& a, afno::Plan& pl) {
     return fail(AFNO_ERR_UNSUPPORTED, "H transform exceeds the per-thread register budget");
 
   pl.spec_bytes = (size_t)a.B * a.H * pl.KW * a.C * 2 * es;
+  pl.frag_offset = (pl.spec_bytes + 255) / 256 * 256;
+  pl.ws_bytes = pl.frag_offset + (afno::use_fast_col(pl) ? afno::frag_bytes(pl) : 0);
 
   // out must not overlap any input
   const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;
@@ -194,11 +196,11 @@ int run(const Args& a, int stage, float* dst, hipStream_t stream) {
   }
 
   void* S = nullptr;
-  e = hipMallocAsync(&S, pl.spec_bytes, stream);
+  e = hipMallocAsync(&S, pl.ws_bytes, stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") +
-                                  std::to_string(pl.spec_bytes) + " bytes: " + hipGetErrorString(e));
+                                  std::to_string(pl.ws_bytes) + " bytes: " + hipGetErrorString(e));
   }
   hipEvent_t* ev = stage == afno::kStageFull ? profile_slot() : nullptr;
   e = afno::launch_filter(pl, a.x, a.w1, a.b1, a.w2, a.b2, S, a.out, dst, stage, stream, ev);

@@ -46,13 +46,17 @@ struct Plan {
   ColParams col;
   size_t row_lds, col_lds;
   int col_threads;
-  size_t spec_bytes;  // workspace: B * H * KW * C complex values
+  size_t spec_bytes;  // spectrum: B * H * KW * C complex values
+  size_t frag_offset; // fragment-ordered weights (size-specialised column kernel), after S
+  size_t ws_bytes;    // whole workspace
 };
 
 hipError_t set_kernel_attributes();
 void set_kernel_path(int path);  // 0: size-specialised kernels where available, 1: generic only
 bool fast_row_available(int64_t W, int64_t C);
 bool fast_col_available(int dtype, int64_t H, int64_t bs);
+bool use_fast_col(const Plan& pl);  // under the current kernel path
+size_t frag_bytes(const Plan& pl);
 // ev: NULL, or 4 events recorded before the first kernel and after each of the three
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,

@@ -78,24 +78,31 @@ static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, 
 
 template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE,
           int NT = ColShape<BS>::kThreads>
-static void launch_col_fast_one(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
-                                const T* b2, int stage, hipStream_t st) {
+static void launch_col_fast_one(const Plan& pl, T* S, const typename FragWord<T>::type* wf,
+                                const T* b1, const T* b2, int stage, hipStream_t st) {
   constexpr int lds = ColLds<T, FT, H, BS>::kBytes;
   constexpr int nthr = NT;
   hipLaunchKernelGGL((column_fast<T, FT, H, N1, N2, BS, WPE, NT>), dim3((unsigned)(pl.B * pl.KW * pl.nb)),
-                     dim3(nthr), lds, st, S, w1, b1, w2, b2, (int)pl.C, (int)pl.KW, (int)pl.nb,
+                     dim3(nthr), lds, st, S, wf, b1, b2, (int)pl.C, (int)pl.KW, (int)pl.nb,
                      (int)pl.kept_h, pl.col.lam, pl.col.inv_sqrt_h, stage);
 }
 
+// Fragment-ordered weights first (into the workspace after the spectrum), then the column
+// kernel reads them with one load per fragment.
 template <typename T>
 static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
                             const T* b2, int stage, hipStream_t st) {
+  typedef typename FragWord<T>::type Word;
+  Word* wf = reinterpret_cast<Word*>(reinterpret_cast<char*>(S) + pl.frag_offset);
+  const int64_t words = pl.nb * frag_words_per_block<T>((int)pl.bs);
+  const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
+  hipLaunchKernelGGL(prep_weights<T>, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs, wf);
   if (pl.H == 16 && pl.bs == 16)
-    launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, w1, b1, w2, b2, stage, st);
+    launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, wf, b1, b2, stage, st);
   else if (pl.H == 90 && pl.bs == 96)
-    launch_col_fast_one<T, float, 90, 9, 10, 96, 4, 512>(pl, S, w1, b1, w2, b2, stage, st);
+    launch_col_fast_one<T, float, 90, 9, 10, 96, 4, 512>(pl, S, wf, b1, b2, stage, st);
   else if constexpr (sizeof(T) == 2)
-    launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, w1, b1, w2, b2, stage, st);
+    launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, wf, b1, b2, stage, st);
 }
 
 // ------------------------------------------------------------------ launchers
@@ -103,6 +110,15 @@ static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, cons
 static int g_kernel_path = 0;  // 0: size-specialised where available, 1: generic only
 
 void set_kernel_path(int path) { g_kernel_path = path; }
+
+bool use_fast_col(const Plan& pl) {
+  return g_kernel_path == 0 && fast_col_available(pl.dtype, pl.H, pl.bs);
+}
+
+size_t frag_bytes(const Plan& pl) {
+  return (size_t)pl.nb * (size_t)(pl.dtype == 0 ? frag_words_per_block<float>((int)pl.bs) * 4
+                                                 : frag_words_per_block<bf16>((int)pl.bs) * 16);
+}
 
 template <typename T>
 static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, const void* b1,
@@ -112,7 +128,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   T* St = static_cast<T*>(S);
   const bool generic = g_kernel_path == 1;
   const bool row_fast = !generic && fast_row_available(pl.W, pl.C);
-  const bool col_fast = !generic && fast_col_available(pl.dtype, pl.H, pl.bs);
+  const bool col_fast = use_fast_col(pl);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
   if (ev) (void)hipEventRecord(ev[0], st);
   if (row_fast)

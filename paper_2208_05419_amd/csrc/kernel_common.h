@@ -114,6 +114,31 @@ template <> struct Mma<float> {
   }
 };
 
+// One lane's B fragment of the real-ified weight in storage form: four dwords (eight bf16)
+// for the bf16 MFMA, one float for the fp32 MFMA.
+template <typename T> struct FragWord;
+template <> struct FragWord<bf16> {
+  typedef uint4 type;
+  __device__ static type make(const bf16* w, int n_out, int kbase, int j, int sg, int lane) {
+    union { Mma<bf16>::Frag f; uint4 u; } r;
+    r.f = Mma<bf16>::load_b(w, n_out, kbase, j, sg, lane);
+    return r.u;
+  }
+};
+template <> struct FragWord<float> {
+  typedef uint32_t type;
+  __device__ static type make(const float* w, int n_out, int kbase, int j, int sg, int lane) {
+    return __float_as_uint(Mma<float>::load_b(w, n_out, kbase, j, sg, lane));
+  }
+};
+
+// Fragment-ordered weights of one block: index ((layer * KSTEPS + s) * NT16 + t) * 64 + lane,
+// k-step s of Mma<T>::kK real inputs, n-tile t of 16 real output columns.
+template <typename T>
+__host__ __device__ constexpr int64_t frag_words_per_block(int bs) {
+  return (int64_t)2 * (2 * bs / (sizeof(T) == 2 ? 32 : 4)) * (2 * bs / 16) * 64;
+}
+
 // hard mode cutoff along H: row kh kept when |signed kh| < kept_h
 __device__ __forceinline__ bool row_kept(int r, int H, int kept_h) {
   if (r >= H) return false;

@@ -248,24 +248,48 @@ struct MlpGrid {
   static_assert(WM * WN == kWaves && MW * WM == MT && NW * WN * 16 == 2 * BS, "MLP wave grid");
 };
 
+// Writes the fragment-ordered weights of both layers of every block (frag_words_per_block
+// words per block): each lane of the column kernel then fetches a whole B fragment with
+// one load at a wave-uniform offset, already permuted and sign-flipped.
+template <typename T>
+__global__ void __launch_bounds__(256)
+prep_weights(const T* __restrict__ w1, const T* __restrict__ w2, int nb, int bs,
+             typename FragWord<T>::type* __restrict__ out) {
+  const int nt16 = 2 * bs / 16, ksteps = 2 * bs / Mma<T>::kK;
+  const int64_t total = (int64_t)nb * frag_words_per_block<T>(bs);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(i & 63);
+    int64_t f = i >> 6;
+    const int t = (int)(f % nt16);
+    f /= nt16;
+    const int s = (int)(f % ksteps);
+    f /= ksteps;
+    const int layer = (int)(f & 1);
+    const int64_t blk = f >> 1;
+    const T* w = (layer ? w2 : w1) + blk * bs * bs * 2;
+    const int j = (16 * t + (lane & 15)) >> 1;
+    out[i] = FragWord<T>::make(w, bs, s * Mma<T>::kK, j, lane & 1, lane);
+  }
+}
+
 // One layer: acc[m][n] = (rows of the wave's m-tile m) x (real-ified complex weight of its
-// n-tile n).  Every m-tile is computed (rows outside the cutoff are zeroed by the caller).
-// Weight fragments are fetched KCH k-steps at a time (a byte permutation per dword turns a
-// complex weight into the two real columns it feeds).
+// n-tile n), the weight fragments read from the prepared buffer wb (this block, this
+// layer).  Every m-tile is computed (rows outside the cutoff are zeroed by the caller).
 template <typename T, int NT, int BS, int MT>
-__device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, int wm, int wn,
+__device__ __forceinline__ void gemm_layer(const T* tile, const Buf& wb, uint32_t layer_off,
+                                           int lane, int wm, int wn,
                                            f32x4 (&acc)[MlpGrid<NT, BS, MT>::MW][MlpGrid<NT, BS, MT>::NW]) {
   typedef Mma<T> M;
   typedef MlpGrid<NT, BS, MT> G;
+  typedef typename FragWord<T>::type Word;
   constexpr int LDT = 2 * BS + (sizeof(T) == 2 ? 8 : 4);
   constexpr int KSTEPS = 2 * BS / M::kK;
+  constexpr int NT16 = 2 * BS / 16;
   constexpr int KCH0 = sizeof(T) == 2 ? 2 : 4;
   constexpr int KCH = KSTEPS < KCH0 ? KSTEPS : KCH0;
   static_assert(KSTEPS % KCH == 0, "k-step chunking");
-  const int sg = lane & 1;
-  int jn[G::NW];
-#pragma unroll
-  for (int n = 0; n < G::NW; ++n) jn[n] = (16 * (wn * G::NW + n) + (lane & 15)) >> 1;
+  const uint32_t voff = lane * (uint32_t)sizeof(Word);
 #pragma unroll
   for (int m = 0; m < G::MW; ++m)
 #pragma unroll
@@ -277,7 +301,17 @@ __device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, 
 #pragma unroll
     for (int s = 0; s < KCH; ++s)
 #pragma unroll
-      for (int n = 0; n < G::NW; ++n) bfr[s][n] = M::load_b(w, BS, (s0 + s) * M::kK, jn[n], sg, lane);
+      for (int n = 0; n < G::NW; ++n) {
+        const uint32_t soff = layer_off + ((s0 + s) * NT16 + wn * G::NW + n) * 64 * (uint32_t)sizeof(Word);
+        if constexpr (sizeof(T) == 2) {
+          union { uint4 u; typename M::Frag f; } r;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, voff, soff, 0);
+          r.u = make_uint4(v[0], v[1], v[2], v[3]);
+          bfr[s][n] = r.f;
+        } else {
+          bfr[s][n] = __uint_as_float(wb.ld32(voff, soff));
+        }
+      }
 #pragma unroll
     for (int s = 0; s < KCH; ++s) {
       typename M::Frag a[G::MW];
@@ -300,8 +334,8 @@ __device__ __forceinline__ void gemm_layer(const T* tile, const T* w, int lane, 
 // stage: 0 full, 1 stop after the forward transform, 2 stop after the MLP.
 template <typename T, typename FT, int H, int N1, int N2, int BS, int WPE, int NT>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE)))
-column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b1,
-            const T* __restrict__ w2, const T* __restrict__ b2, int C, int KW, int nb,
+column_fast(T* __restrict__ S, const typename FragWord<T>::type* __restrict__ wfrag,
+            const T* __restrict__ b1, const T* __restrict__ b2, int C, int KW, int nb,
             int kept_h, float lam, float scale, int stage) {
   static_assert(N1 * N2 == H, "H = N1 N2");
   static_assert(BS % 16 == 0, "block size multiple of 16");
@@ -388,15 +422,16 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
     // ---- block MLP on the wave grid
     typedef MlpGrid<NT, BS, MT> G;
     const int wm = wave / G::WN, wn = wave % G::WN;
-    const T* W1 = w1 + (int64_t)blk * BS * BS * 2;
-    const T* W2 = w2 + (int64_t)blk * BS * BS * 2;
+    constexpr int64_t kBlockWords = frag_words_per_block<T>(BS);
+    const Buf wb(wfrag + blk * kBlockWords, (uint32_t)(kBlockWords * sizeof(typename FragWord<T>::type)));
+    constexpr uint32_t kLayerBytes = (uint32_t)(kBlockWords / 2 * sizeof(typename FragWord<T>::type));
     const T* B1 = b1 + (int64_t)blk * BS * 2;
     const T* B2 = b2 + (int64_t)blk * BS * 2;
     const int col0 = 16 * G::NW * wn + (lane & 15);  // real output column of n-tile 0
     const int row0 = 16 * G::MW * wm + 4 * (lane >> 4);
     const bool all_rows = kept_h > H / 2;  // cutoff keeps every row
     f32x4 acc[G::MW][G::NW];
-    gemm_layer<T, NT, BS, MT>(tile, W1, lane, wm, wn, acc);
+    gemm_layer<T, NT, BS, MT>(tile, wb, 0, lane, wm, wn, acc);
     float bias[G::NW];
 #pragma unroll
     for (int n = 0; n < G::NW; ++n) bias[n] = ld_f(B1 + col0 + 16 * n);
@@ -410,7 +445,7 @@ column_fast(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b
           tile[(row0 + 16 * m + r) * LDT + col0 + 16 * n] =
               Store<T>::to(fmaxf(acc[m][n][r] + bias[n], 0.f));
     __syncthreads();  // hidden layer complete
-    gemm_layer<T, NT, BS, MT>(tile, W2, lane, wm, wn, acc);
+    gemm_layer<T, NT, BS, MT>(tile, wb, kLayerBytes, lane, wm, wn, acc);
 #pragma unroll
     for (int n = 0; n < G::NW; ++n) bias[n] = ld_f(B2 + col0 + 16 * n);
     __syncthreads();  // every wave has read its hidden rows
