@@ -104,7 +104,7 @@ int make_plan(const Args& a, afno::Plan& pl) {
   if (a.H > 16 * afno::kColMaxMTiles)
     return fail(AFNO_ERR_UNSUPPORTED, "H must be <= 192");
   const double elems = (double)a.B * a.H * a.W * a.C;
-  if (elems > 4.0e15 || (double)a.B * a.H > 2.0e9 || (double)a.B * Wm * a.nb > 2.0e9)
+  if (elems > 4.0e15 || (double)a.B * a.H * (a.C / 16) > 2.0e9 || (double)a.B * Wm * a.nb > 2.0e9)
     return fail(AFNO_ERR_UNSUPPORTED, "tensor too large");
 
   // W-axis workgroups: rc channels, rc/2 complex signals

@@ -53,7 +53,7 @@ static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, hipStream_t st
   const float sc = 0.5f * pl.row.inv_sqrt_w;
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
-    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(gx, (unsigned)(pl.C / (2 * np))), \
+    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(gx * (unsigned)(pl.C / (2 * np))), \
                        dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc);            \
     return;                                                                               \
   }
@@ -68,7 +68,7 @@ static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, 
   const float sc = pl.row.inv_sqrt_w;
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
-    hipLaunchKernelGGL((row_c2r_fast<T, w, n1, n2, np>), dim3(gx, (unsigned)(pl.C / (2 * np))), \
+    hipLaunchKernelGGL((row_c2r_fast<T, w, n1, n2, np>), dim3(gx * (unsigned)(pl.C / (2 * np))), \
                        dim3(np * n1), 0, st, S, x, out, dst, (int)pl.C, (int)pl.KW, sc, mode); \
     return;                                                                               \
   }

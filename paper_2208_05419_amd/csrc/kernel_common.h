@@ -167,6 +167,18 @@ struct Buf {
   __device__ __forceinline__ void st32(uint32_t v, uint32_t voff, uint32_t soff) const {
     __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
   }
+  __device__ __forceinline__ uint2 ld64(uint32_t voff, uint32_t soff) const {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    return make_uint2(v[0], v[1]);
+  }
+  __device__ __forceinline__ void st64(uint2 v, uint32_t voff, uint32_t soff) const {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(u2{v.x, v.y}, r, voff, soff, 0);
+  }
+  __device__ __forceinline__ void st128(uint4 v, uint32_t voff, uint32_t soff) const {
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(u4{v.x, v.y, v.z, v.w}, r, voff, soff, 0);
+  }
 };
 __device__ __forceinline__ uint32_t buf_bytes(uint64_t n) {
   return n >= 0xffffffffull ? 0xffffffffu : (uint32_t)n;

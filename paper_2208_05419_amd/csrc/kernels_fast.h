@@ -73,15 +73,52 @@ template <> struct CBuf<float> {
   }
 };
 
+// two consecutive real channels (c, c+1) through a buffer, as the complex value x_c + i x_{c+1}
+__device__ __forceinline__ float2 ld_pair(const Buf& b, const float*, uint32_t voff, uint32_t soff) {
+  const uint2 v = b.ld64(voff, soff);
+  return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+}
+__device__ __forceinline__ float2 ld_pair(const Buf& b, const bf16*, uint32_t voff, uint32_t soff) {
+  return widen2(b.ld32(voff, soff));
+}
+__device__ __forceinline__ void st_pair(const Buf& b, const float*, uint32_t voff, uint32_t soff, float2 v) {
+  b.st64(make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)), voff, soff);
+}
+__device__ __forceinline__ void st_pair(const Buf& b, const bf16*, uint32_t voff, uint32_t soff, float2 v) {
+  b.st32(pack_c(v, (const bf16*)nullptr), voff, soff);
+}
+__device__ __forceinline__ typename Raw2<float>::type ld_raw_pair(const Buf& b, const float*, uint32_t voff, uint32_t soff) {
+  return ld_pair(b, (const float*)nullptr, voff, soff);
+}
+__device__ __forceinline__ typename Raw2<bf16>::type ld_raw_pair(const Buf& b, const bf16*, uint32_t voff, uint32_t soff) {
+  return b.ld32(voff, soff);
+}
+// two complex values (re, im of channel c, re, im of channel c+1)
+__device__ __forceinline__ float4 ld_cpair(const Buf& b, const float*, uint32_t voff, uint32_t soff) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(b.r, voff, soff, 0);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
+__device__ __forceinline__ float4 ld_cpair(const Buf& b, const bf16*, uint32_t voff, uint32_t soff) {
+  const uint2 v = b.ld64(voff, soff);
+  const float2 a = widen2(v.x), c = widen2(v.y);
+  return make_float4(a.x, a.y, c.x, c.y);
+}
+__device__ __forceinline__ void st_cpair(const Buf& b, const float*, uint32_t voff, uint32_t soff, float4 v) {
+  b.st128(make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)), voff, soff);
+}
+__device__ __forceinline__ void st_cpair(const Buf& b, const bf16*, uint32_t voff, uint32_t soff, float4 v) {
+  b.st64(make_uint2(pack_c(make_float2(v.x, v.y), (const bf16*)nullptr),
+                    pack_c(make_float2(v.z, v.w), (const bf16*)nullptr)), voff, soff);
+}
+
 // X_c = (Z[k] + conj Z[W-k]) s,  X_{c+1} = (Z[k] - conj Z[W-k]) s / i  with s = 1/(2 sqrt W)
-template <typename T>
-__device__ __forceinline__ void store_split(T* o, float2 z, float2 zm, float s) {
-  st_c2(o, make_float4((z.x + zm.x) * s, (z.y - zm.y) * s, (z.y + zm.y) * s, (zm.x - z.x) * s));
+__device__ __forceinline__ float4 split_pair(float2 z, float2 zm, float s) {
+  return make_float4((z.x + zm.x) * s, (z.y - zm.y) * s, (z.y + zm.y) * s, (zm.x - z.x) * s);
 }
 
 // ------------------------------------------------------------------ W-axis forward
 
-// grid (B * H, C / (2 NP)), block NP * N1.  NP complex signals (2 NP channels) per
+// grid B * H * C / (2 NP), block NP * N1.  NP complex signals (2 NP channels) per
 // workgroup; signal p of thread t = t % NP.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
@@ -91,14 +128,21 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
   __shared__ float2 F[N2 * N1 * NP];
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;  // b * H + h
-  const int c0 = blockIdx.y * (2 * NP);
+  // consecutive workgroups take consecutive channel chunks of one row (DRAM page locality)
+  const int nchunk = C / (2 * NP);
+  const int64_t row = blockIdx.x / nchunk;  // b * H + h
+  const int c0 = (int)(blockIdx.x % nchunk) * (2 * NP);
+  constexpr uint32_t es = sizeof(T);
+  const uint32_t xrow = (uint32_t)C * es;        // bytes between consecutive w
+  const uint32_t srow = (uint32_t)C * 2 * es;    // bytes between consecutive kw of S
+  const Buf xb(x + row * (int64_t)W * C + c0, (uint32_t)W * xrow);
+  const Buf sb(S + (row * (int64_t)KW * C + c0) * 2, (uint32_t)KW * srow);
   {
     const int p = tid % NP, j = tid / NP;
-    const T* xr = x + row * (int64_t)W * C + c0 + 2 * p;
+    const uint32_t voff = 2 * p * es + j * xrow;
     float2 v[N2];
 #pragma unroll
-    for (int t = 0; t < N2; ++t) v[t] = ld_c(xr + (int64_t)(j + N1 * t) * C);
+    for (int t = 0; t < N2; ++t) v[t] = ld_pair(xb, (const T*)nullptr, voff, N1 * t * xrow);
     fill_roots<W, NT>(tw);
     __syncthreads();
     DftReg<N2, false>::run(v);
@@ -121,23 +165,24 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
     }
     DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
     DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
-    T* Sr = S + row * (int64_t)KW * C * 2 + (int64_t)(c0 + 2 * p) * 2;
+    const uint32_t va = 4 * p * es + qa * srow, vb = 4 * p * es + qb * srow;
 #pragma unroll
     for (int k1 = 0; k1 < N1; ++k1) {
       // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
       const int ka = qa + N2 * k1;
       const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
-      if (ka <= W / 2 && ka < KW) store_split(Sr + (int64_t)ka * C * 2, a[k1], zam, scale);
+      if (ka <= W / 2 && ka < KW)
+        st_cpair(sb, (const T*)nullptr, va, N2 * k1 * srow, split_pair(a[k1], zam, scale));
       const int kb = qb + N2 * k1;
       if (qb != qa && kb <= W / 2 && kb < KW)
-        store_split(Sr + (int64_t)kb * C * 2, b[k1], a[N1 - 1 - k1], scale);
+        st_cpair(sb, (const T*)nullptr, vb, N2 * k1 * srow, split_pair(b[k1], a[N1 - 1 - k1], scale));
     }
   }
 }
 
 // ------------------------------------------------------------------ W-axis inverse + residual
 
-// grid (B * H, C / (2 NP)), block NP * N1.  mode 0: out = x + y (dtype T); mode 1: dst = y.
+// grid B * H * C / (2 NP), block NP * N1.  mode 0: out = x + y (dtype T); mode 1: dst = y.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
 row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ out,
@@ -149,8 +194,17 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
   __shared__ float2 F[N2 * N1 * NP];
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
-  const int c0 = blockIdx.y * (2 * NP);
+  const int nchunk = C / (2 * NP);
+  const int64_t row = blockIdx.x / nchunk;
+  const int c0 = (int)(blockIdx.x % nchunk) * (2 * NP);
+  constexpr uint32_t es = sizeof(T);
+  const uint32_t xrow = (uint32_t)C * es;
+  const uint32_t srow = (uint32_t)C * 2 * es;
+  const int64_t xbase = row * (int64_t)W * C + c0;
+  const Buf xb(x + xbase, (uint32_t)W * xrow);
+  const Buf ob(out + xbase, (uint32_t)W * xrow);
+  const Buf db(dst + xbase, (uint32_t)W * C * 4);
+  const Buf sb(S + (row * (int64_t)KW * C + c0) * 2, (uint32_t)KW * srow);
   // the residual of the second-stage tasks, fetched first so its latency overlaps the
   // transform (kept in storage form)
   typename Raw2<T>::type xres[TP2][N1];
@@ -160,15 +214,14 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
       const int task = tid + u * NT;
       if (task < NP * N2) {
         const int p = task % NP, k2 = task / NP;
-        const T* xr = x + row * (int64_t)W * C + c0 + 2 * p;
+        const uint32_t voff = 2 * p * es + k2 * xrow;
 #pragma unroll
-        for (int k1 = 0; k1 < N1; ++k1) xres[u][k1] = ld_raw2(xr + (int64_t)(k2 + N2 * k1) * C);
+        for (int k1 = 0; k1 < N1; ++k1) xres[u][k1] = ld_raw_pair(xb, (const T*)nullptr, voff, N2 * k1 * xrow);
       }
     }
   }
   {
     const int p = tid % NP, j = tid / NP;
-    const T* Sr = S + row * (int64_t)KW * C * 2 + (int64_t)(c0 + 2 * p) * 2;
     float2 v[N2];
 #pragma unroll
     for (int t = 0; t < N2; ++t) {
@@ -177,7 +230,7 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
       const int k = j + N1 * t;
       const int kk = k <= HALF ? k : W - k;
       float4 y = make_float4(0.f, 0.f, 0.f, 0.f);  // (Re Y_c, Im Y_c, Re Y_c+1, Im Y_c+1)
-      if (kk < KW) y = ld_c2(Sr + (int64_t)kk * C * 2);
+      if (kk < KW) y = ld_cpair(sb, (const T*)nullptr, 4 * p * es + kk * srow, 0);
       v[t] = (k == 0 || k == HALF) ? make_float2(y.x, y.z)
              : (k < HALF ? make_float2(y.x - y.w, y.y + y.z) : make_float2(y.x + y.w, y.z - y.y));
     }
@@ -198,16 +251,15 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
 #pragma unroll
     for (int j = 0; j < N1; ++j) a[j] = F[(k2 * N1 + j) * NP + p];
     DftReg<N1, true>::run(a);  // a[k1] = z[k2 + N2 k1] = y_c + i y_{c+1}
-    const int64_t base = row * (int64_t)W * C + c0 + 2 * p;
+    const uint32_t voff = 2 * p * es + k2 * xrow, dvoff = 2 * p * 4 + k2 * C * 4;
 #pragma unroll
     for (int k1 = 0; k1 < N1; ++k1) {
-      const int64_t off = base + (int64_t)(k2 + N2 * k1) * C;
       const float2 y = make_float2(a[k1].x * scale, a[k1].y * scale);
       if (mode == 1) {
-        *reinterpret_cast<float2*>(dst + off) = y;
+        st_pair(db, (const float*)nullptr, dvoff, N2 * k1 * C * 4, y);
       } else {
         const float2 xv = widen2(xres[u][k1]);
-        st_c(out + off, make_float2(xv.x + y.x, xv.y + y.y));
+        st_pair(ob, (const T*)nullptr, voff, N2 * k1 * xrow, make_float2(xv.x + y.x, xv.y + y.y));
       }
     }
   }
