@@ -183,6 +183,9 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
 // ------------------------------------------------------------------ W-axis inverse + residual
 
 // grid B * H * C / (2 NP), block NP * N1.  mode 0: out = x + y (dtype T); mode 1: dst = y.
+// Global traffic goes through LDS in 16-byte vectors: the kept half spectrum of the
+// workgroup's 2 NP channels is staged once (each stored bin feeds both Z[k] and Z[W-k]),
+// the residual is prefetched at kernel start, and the output leaves in 16-byte stores.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
 row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ out,
@@ -190,14 +193,19 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
   static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
   constexpr int NT = NP * N1;
   constexpr int HALF = W / 2;
-  constexpr int TP2 = (NP * N2 + NT - 1) / NT;  // second-stage tasks per thread
-  __shared__ float2 F[N2 * N1 * NP];
+  constexpr uint32_t es = sizeof(T);
+  constexpr int XV = 16 / es;                          // channels per 16-byte vector of x / out
+  constexpr int XPR = 2 * NP / XV;                     // 16-byte vectors per row of the slice
+  constexpr int TX = (W * XPR + NT - 1) / NT;          // residual vectors per thread
+  constexpr int SPR = 2 * NP * 2 * es / 16;            // 16-byte vectors per spectrum row
+  constexpr int TP2 = (NP * N2 + NT - 1) / NT;         // second-stage tasks per thread
+  constexpr int FN = (HALF + 1) * SPR * 2 > W * NP ? (HALF + 1) * SPR * 2 : W * NP;
+  __shared__ float2 F[FN];                             // staged spectrum / stage-1 output / y
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
   const int nchunk = C / (2 * NP);
   const int64_t row = blockIdx.x / nchunk;
   const int c0 = (int)(blockIdx.x % nchunk) * (2 * NP);
-  constexpr uint32_t es = sizeof(T);
   const uint32_t xrow = (uint32_t)C * es;
   const uint32_t srow = (uint32_t)C * 2 * es;
   const int64_t xbase = row * (int64_t)W * C + c0;
@@ -205,62 +213,120 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
   const Buf ob(out + xbase, (uint32_t)W * xrow);
   const Buf db(dst + xbase, (uint32_t)W * C * 4);
   const Buf sb(S + (row * (int64_t)KW * C + c0) * 2, (uint32_t)KW * srow);
-  // the residual of the second-stage tasks, fetched first so its latency overlaps the
-  // transform (kept in storage form)
-  typename Raw2<T>::type xres[TP2][N1];
-  if (mode == 0) {
+  uint4* F4 = reinterpret_cast<uint4*>(F);
+  // ---- the kept half spectrum of the slice and the residual, 16-byte loads
+  {
+    uint4 sv[((HALF + 1) * SPR + NT - 1) / NT];
 #pragma unroll
-    for (int u = 0; u < TP2; ++u) {
-      const int task = tid + u * NT;
-      if (task < NP * N2) {
-        const int p = task % NP, k2 = task / NP;
-        const uint32_t voff = 2 * p * es + k2 * xrow;
-#pragma unroll
-        for (int k1 = 0; k1 < N1; ++k1) xres[u][k1] = ld_raw_pair(xb, (const T*)nullptr, voff, N2 * k1 * xrow);
+    for (int u = 0; u < ((HALF + 1) * SPR + NT - 1) / NT; ++u) {
+      const int i = tid + u * NT;
+      const int r = i / SPR, v = i % SPR;
+      sv[u] = make_uint4(0, 0, 0, 0);
+      if (r < KW && r <= HALF) {
+        const auto q = __builtin_amdgcn_raw_buffer_load_b128(sb.r, v * 16 + r * srow, 0, 0);
+        sv[u] = make_uint4(q[0], q[1], q[2], q[3]);
       }
     }
+    fill_roots<W, NT>(tw);
+#pragma unroll
+    for (int u = 0; u < ((HALF + 1) * SPR + NT - 1) / NT; ++u) {
+      const int i = tid + u * NT;
+      if (i < (HALF + 1) * SPR) F4[i] = sv[u];  // row r of the stored half at r * SPR
+    }
   }
+  uint4 xres[TX];
+  if (mode == 0) {
+#pragma unroll
+    for (int u = 0; u < TX; ++u) {
+      const int i = min(tid + u * NT, W * XPR - 1);
+      const auto q = __builtin_amdgcn_raw_buffer_load_b128(xb.r, (i % XPR) * 16 + (i / XPR) * xrow, 0, 0);
+      xres[u] = make_uint4(q[0], q[1], q[2], q[3]);
+    }
+  }
+  __syncthreads();
+  // ---- first stage: task (p, j) gathers Z[j + N1 t] from the staged half spectrum
+  float2 v[N2];
+  const int p = tid % NP, j = tid / NP;
   {
-    const int p = tid % NP, j = tid / NP;
-    float2 v[N2];
+    const char* Fb = reinterpret_cast<const char*>(F);
 #pragma unroll
     for (int t = 0; t < N2; ++t) {
-      // Z[k] = Y_c[k] + i Y_{c+1}[k] over the full length from the stored half:
-      // Y[W - k] = conj Y[k]; only the real parts of the k = 0 and k = W/2 bins count.
+      // Z[k] = Y_c[k] + i Y_{c+1}[k] over the full length: Y[W - k] = conj Y[k]; only the
+      // real parts of the k = 0 and k = W/2 bins count
       const int k = j + N1 * t;
       const int kk = k <= HALF ? k : W - k;
-      float4 y = make_float4(0.f, 0.f, 0.f, 0.f);  // (Re Y_c, Im Y_c, Re Y_c+1, Im Y_c+1)
-      if (kk < KW) y = ld_cpair(sb, (const T*)nullptr, 4 * p * es + kk * srow, 0);
+      float4 y;
+      if constexpr (es == 2) {
+        const uint2 q = *reinterpret_cast<const uint2*>(Fb + kk * SPR * 16 + p * 8);
+        const float2 a = widen2(q.x), c = widen2(q.y);
+        y = make_float4(a.x, a.y, c.x, c.y);
+      } else {
+        y = *reinterpret_cast<const float4*>(Fb + kk * SPR * 16 + p * 16);
+      }
       v[t] = (k == 0 || k == HALF) ? make_float2(y.x, y.z)
              : (k < HALF ? make_float2(y.x - y.w, y.y + y.z) : make_float2(y.x + y.w, y.z - y.y));
     }
-    fill_roots<W, NT>(tw);
-    __syncthreads();
-    DftReg<N2, true>::run(v);
+  }
+  __syncthreads();  // the staged spectrum has been read; F is overwritten below
+  DftReg<N2, true>::run(v);
 #pragma unroll
-    for (int k2 = 0; k2 < N2; ++k2)
-      F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<true>(v[k2], tw, (j * k2) % W);
+  for (int k2 = 0; k2 < N2; ++k2)
+    F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<true>(v[k2], tw, (j * k2) % W);
+  __syncthreads();
+  // ---- second stage: task (p, k2) -> y at w = k2 + N2 k1, held until F is free
+  float2 yv[TP2][N1];
+#pragma unroll
+  for (int u = 0; u < TP2; ++u) {
+    const int task = min(tid + u * NT, NP * N2 - 1);
+    const int pp = task % NP, k2 = task / NP;
+#pragma unroll
+    for (int jj = 0; jj < N1; ++jj) yv[u][jj] = F[(k2 * N1 + jj) * NP + pp];
   }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < TP2; ++u) {
     const int task = tid + u * NT;
-    if (task >= NP * N2) break;
-    const int p = task % NP, k2 = task / NP;
-    float2 a[N1];
+    if (task < NP * N2) {
+      const int pp = task % NP, k2 = task / NP;
+      DftReg<N1, true>::run(yv[u]);  // yv[k1] = z[k2 + N2 k1] = y_c + i y_{c+1}
 #pragma unroll
-    for (int j = 0; j < N1; ++j) a[j] = F[(k2 * N1 + j) * NP + p];
-    DftReg<N1, true>::run(a);  // a[k1] = z[k2 + N2 k1] = y_c + i y_{c+1}
-    const uint32_t voff = 2 * p * es + k2 * xrow, dvoff = 2 * p * 4 + k2 * C * 4;
+      for (int k1 = 0; k1 < N1; ++k1) F[(k2 + N2 * k1) * NP + pp] = yv[u][k1];  // y[w][pair]
+    }
+  }
+  __syncthreads();
+  // ---- out = x + y / sqrt(W) (or dst = y), 16-byte vectors along each row
+  if (mode == 0) {
 #pragma unroll
-    for (int k1 = 0; k1 < N1; ++k1) {
-      const float2 y = make_float2(a[k1].x * scale, a[k1].y * scale);
-      if (mode == 1) {
-        st_pair(db, (const float*)nullptr, dvoff, N2 * k1 * C * 4, y);
-      } else {
-        const float2 xv = widen2(xres[u][k1]);
-        st_pair(ob, (const T*)nullptr, voff, N2 * k1 * xrow, make_float2(xv.x + y.x, xv.y + y.y));
+    for (int u = 0; u < TX; ++u) {
+      const int i = tid + u * NT;
+      if (i < W * XPR) {
+        const int w = i / XPR, g = i % XPR;
+        const float* yr = reinterpret_cast<const float*>(F + w * NP) + g * XV;  // XV channels
+        union { uint4 u4; uint32_t w32[4]; } xo, ov;
+        xo.u4 = xres[u];
+        if constexpr (es == 2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float2 xv = widen2(xo.w32[e]);
+            ov.w32[e] = pack_c(make_float2(xv.x + yr[2 * e] * scale, xv.y + yr[2 * e + 1] * scale),
+                               (const bf16*)nullptr);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            ov.w32[e] = __float_as_uint(__uint_as_float(xo.w32[e]) + yr[e] * scale);
+        }
+        ob.st128(ov.u4, g * 16 + w * xrow, 0);
       }
+    }
+  } else {
+    constexpr int DPR = 2 * NP / 4;  // 16-byte float vectors per row of dst
+    for (int i = tid; i < W * DPR; i += NT) {
+      const int w = i / DPR, g = i % DPR;
+      const float4 y = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(F + w * NP) + 4 * g);
+      db.st128(make_uint4(__float_as_uint(y.x * scale), __float_as_uint(y.y * scale),
+                          __float_as_uint(y.z * scale), __float_as_uint(y.w * scale)),
+               g * 16 + w * (uint32_t)C * 4, 0);
     }
   }
 }
