@@ -120,13 +120,17 @@ int afno_profile_end(double* kernel_ms, int64_t* calls);
 
 /*
  * Diagnostic kernel selection, process-wide.  AFNO_PATH_AUTO (the default) runs the
- * size-specialised kernels where the library has them (W in {32, 180, 360}; H x bs in
- * {16 x 16, 90 x 96, 180 x 128 (bf16)}) and the size-generic kernels elsewhere;
- * AFNO_PATH_GENERIC runs the size-generic kernels for every shape.  Both compute the
- * same filter.  Returns AFNO_OK or AFNO_ERR_INVALID_ARG.  Not for use while calls are
- * being enqueued from other threads.
+ * specialised kernels where the library has them and the size-generic kernels elsewhere:
+ * W-axis kernels for W in {32, 180, 360}; for bf16 with H <= 96 and bs in {32, 64, 96}
+ * the column kernel that computes the H-axis DFTs as bf16 matrix-core products against a
+ * DFT table; else column kernels with vector-ALU FFTs for H x bs in {16 x 16, 90 x 96,
+ * 180 x 128 (bf16)}.  AFNO_PATH_VALU_DFT is AUTO without the matrix-core DFT column
+ * kernel; AFNO_PATH_GENERIC runs the size-generic kernels for every shape.  All compute
+ * the same filter (the matrix-core DFT rounds its table to bf16: one more bf16-sized
+ * error per H transform).  Returns AFNO_OK or AFNO_ERR_INVALID_ARG.  Not for use while
+ * calls are being enqueued from other threads.
  */
-enum { AFNO_PATH_AUTO = 0, AFNO_PATH_GENERIC = 1 };
+enum { AFNO_PATH_AUTO = 0, AFNO_PATH_GENERIC = 1, AFNO_PATH_VALU_DFT = 2 };
 int afno_set_kernel_path(int path);
 
 /* Message of the calling thread's last non-OK return ("" if none).  The pointer

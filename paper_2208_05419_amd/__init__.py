@@ -7,7 +7,7 @@ Python binding.  Importing it loads nothing; the library is loaded on first use.
 """
 from .afno import (AFNO_DTYPE_BF16, AFNO_DTYPE_FP32, AFNO_ERR_ALIAS, AFNO_ERR_HIP,  # noqa: F401
                    AFNO_ERR_INVALID_ARG, AFNO_ERR_UNSUPPORTED, AFNO_OK, AFNO_PATH_AUTO,
-                   AFNO_PATH_GENERIC, AFNO_STAGE_DELTA,
+                   AFNO_PATH_GENERIC, AFNO_PATH_VALU_DFT, AFNO_STAGE_DELTA,
                    AFNO_STAGE_MIXED, AFNO_STAGE_SPECTRUM, EXPORTED, LIB_PATH, AfnoError,
                    KERNELS, afno_filter_forward, afno_filter_stage, afno_last_error,
                    afno_profile_begin, afno_profile_end, afno_set_kernel_path, afno_version,

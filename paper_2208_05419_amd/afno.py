@@ -25,6 +25,7 @@ AFNO_STAGE_DELTA = 3
 
 AFNO_PATH_AUTO = 0
 AFNO_PATH_GENERIC = 1
+AFNO_PATH_VALU_DFT = 2
 
 EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_profile_begin", "afno_profile_end",
             "afno_set_kernel_path", "afno_last_error", "afno_version")
@@ -111,7 +112,9 @@ def afno_set_kernel_path(path: int) -> int:
 
 
 def set_kernel_path(path: int):
-    """AFNO_PATH_AUTO: size-specialised kernels where available; AFNO_PATH_GENERIC: generic only."""
+    """AFNO_PATH_AUTO: specialised kernels where available (bf16 columns with H <= 96 and
+    block size 32, 64 or 96 take the matrix-core DFT kernel); AFNO_PATH_VALU_DFT: the same
+    without the matrix-core DFT kernel; AFNO_PATH_GENERIC: generic kernels only."""
     _check(afno_set_kernel_path(path))
 
 

@@ -141,7 +141,10 @@ int make_plan(const Args& a, afno::Plan& pl) {
 
   pl.spec_bytes = (size_t)a.B * a.H * pl.KW * a.C * 2 * es;
   pl.frag_offset = (pl.spec_bytes + 255) / 256 * 256;
-  pl.ws_bytes = pl.frag_offset + (afno::use_fast_col(pl) ? afno::frag_bytes(pl) : 0);
+  const bool mfma = afno::use_mfma_col(pl);
+  const size_t fb = (mfma || afno::use_fast_col(pl)) ? afno::frag_bytes(pl) : 0;
+  pl.tab_offset = (pl.frag_offset + fb + 255) / 256 * 256;
+  pl.ws_bytes = mfma ? pl.tab_offset + afno::mfma_tab_bytes(pl) : pl.frag_offset + fb;
 
   // out must not overlap any input
   const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;
@@ -290,8 +293,9 @@ int afno_profile_end(double* kernel_ms, int64_t* calls) {
 
 int afno_set_kernel_path(int path) {
   g_last_error.clear();
-  if (path != AFNO_PATH_AUTO && path != AFNO_PATH_GENERIC)
-    return fail(AFNO_ERR_INVALID_ARG, "path must be AFNO_PATH_AUTO or AFNO_PATH_GENERIC");
+  if (path != AFNO_PATH_AUTO && path != AFNO_PATH_GENERIC && path != AFNO_PATH_VALU_DFT)
+    return fail(AFNO_ERR_INVALID_ARG,
+                "path must be AFNO_PATH_AUTO, AFNO_PATH_GENERIC or AFNO_PATH_VALU_DFT");
   afno::set_kernel_path(path);
   return AFNO_OK;
 }

@@ -47,16 +47,22 @@ struct Plan {
   size_t row_lds, col_lds;
   int col_threads;
   size_t spec_bytes;  // spectrum: B * H * KW * C complex values
-  size_t frag_offset; // fragment-ordered weights (size-specialised column kernel), after S
+  size_t frag_offset; // fragment-ordered weights (size-specialised column kernels), after S
+  size_t tab_offset;  // transform table (MFMA-transform column kernel), after the weights
   size_t ws_bytes;    // whole workspace
 };
 
 hipError_t set_kernel_attributes();
-void set_kernel_path(int path);  // 0: size-specialised kernels where available, 1: generic only
+// 0: specialised kernels where available, 1: generic only, 2: as 0 without the
+// MFMA-transform column kernel
+void set_kernel_path(int path);
 bool fast_row_available(int64_t W, int64_t C);
 bool fast_col_available(int dtype, int64_t H, int64_t bs);
+bool mfma_col_available(int dtype, int64_t H, int64_t bs);
+bool use_mfma_col(const Plan& pl);  // under the current kernel path
 bool use_fast_col(const Plan& pl);  // under the current kernel path
 size_t frag_bytes(const Plan& pl);
+size_t mfma_tab_bytes(const Plan& pl);
 // ev: NULL, or 4 events recorded before the first kernel and after each of the three
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,

@@ -24,6 +24,7 @@
 #include "afno_internal.h"
 #include "kernels_fast.h"
 #include "kernels_generic.h"
+#include "kernels_mfma.h"
 
 namespace afno {
 
@@ -31,7 +32,9 @@ namespace afno {
 //
 // W-axis kernels: W = N1 N2, NP complex signals (2 NP channels) per workgroup.
 //   W = 32: 8 x 4, NP 32;  W = 180: 12 x 15, NP 32;  W = 360: 24 x 15, NP 16.
-// Column kernel: H = N1 N2 with block size BS.
+// Column kernel, bf16 with H <= 96 and BS in {32, 64, 96}: H transforms as MFMA products
+//   against a transform table (kernels_mfma.h), H padded to HP in {32, 64, 96}.
+// Column kernel, vector-ALU transforms: H = N1 N2 with block size BS.
 //   H = 16, BS = 16: 4 x 4;  H = 90, BS = 96: 9 x 10;  H = 180, BS = 128: 12 x 15 (bf16 only,
 //   with a bf16 transform intermediate: a float one would not fit the LDS).
 #define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
@@ -105,14 +108,58 @@ static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, cons
     launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, wf, b1, b2, stage, st);
 }
 
+#define AFNO_MFMA_COL_LIST(X) \
+  X(32, 32) X(32, 64) X(32, 96) X(64, 32) X(64, 64) X(64, 96) X(96, 32) X(96, 64) X(96, 96)
+
+int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
+
+bool mfma_col_available(int dtype, int64_t H, int64_t bs) {
+  return dtype == 1 && H <= 96 && (bs == 32 || bs == 64 || bs == 96);
+}
+
+size_t mfma_tab_bytes(const Plan& pl) {
+  const int hp = mfma_col_hp(pl.H);
+  return (size_t)(2 * hp / 32) * (hp / 16) * 64 * 16;
+}
+
+// Fragment-ordered weights and the transform table into the workspace (one launch), then
+// the column kernel.
+static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* w1, const bf16* b1,
+                            const bf16* w2, const bf16* b2, int stage, hipStream_t st) {
+  uint4* wf = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.frag_offset);
+  uint4* tab = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.tab_offset);
+  const int hp = mfma_col_hp(pl.H);
+  const int64_t words = pl.nb * frag_words_per_block<bf16>((int)pl.bs) + (int64_t)(mfma_tab_bytes(pl) / 16);
+  const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
+  hipLaunchKernelGGL(prep_col_mfma, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs,
+                     (int)pl.H, hp, wf, tab);
+  const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
+#define AFNO_CASE(HP_, BS_)                                                                 \
+  if (hp == HP_ && pl.bs == BS_) {                                                          \
+    constexpr int lds = MfmaCol<HP_, BS_>::kBytes;                                          \
+    hipLaunchKernelGGL((column_mfma<HP_, BS_>), grid, dim3(512), lds, st,                  \
+                       S, wf, tab, b1, b2, (int)pl.H, (int)pl.C, (int)pl.KW, (int)pl.nb,   \
+                       (int)pl.kept_h, pl.col.lam, stage);                                  \
+    return;                                                                                 \
+  }
+  AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
+}
+
 // ------------------------------------------------------------------ launchers
 
-static int g_kernel_path = 0;  // 0: size-specialised where available, 1: generic only
+// 0: MFMA-transform column kernel, else size-specialised, else generic; 1: generic only;
+// 2: as 0 without the MFMA-transform column kernel
+static int g_kernel_path = 0;
 
 void set_kernel_path(int path) { g_kernel_path = path; }
 
+bool use_mfma_col(const Plan& pl) {
+  return g_kernel_path == 0 && mfma_col_available(pl.dtype, pl.H, pl.bs);
+}
+
 bool use_fast_col(const Plan& pl) {
-  return g_kernel_path == 0 && fast_col_available(pl.dtype, pl.H, pl.bs);
+  return g_kernel_path != 1 && !use_mfma_col(pl) && fast_col_available(pl.dtype, pl.H, pl.bs);
 }
 
 size_t frag_bytes(const Plan& pl) {
@@ -128,6 +175,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   T* St = static_cast<T*>(S);
   const bool generic = g_kernel_path == 1;
   const bool row_fast = !generic && fast_row_available(pl.W, pl.C);
+  const bool col_mfma = use_mfma_col(pl);
   const bool col_fast = use_fast_col(pl);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
   if (ev) (void)hipEventRecord(ev[0], st);
@@ -139,7 +187,11 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], st);
   const int col_stage = (stage == kStageSpectrum) ? 1 : (stage == kStageMixed ? 2 : 0);
-  if (col_fast)
+  if (col_mfma) {
+    if constexpr (sizeof(T) == 2)  // mfma_col_available admits bf16 only
+      launch_col_mfma(pl, St, static_cast<const bf16*>(w1), static_cast<const bf16*>(b1),
+                      static_cast<const bf16*>(w2), static_cast<const bf16*>(b2), col_stage, st);
+  } else if (col_fast)
     launch_col_fast<T>(pl, St, static_cast<const T*>(w1), static_cast<const T*>(b1),
                        static_cast<const T*>(w2), static_cast<const T*>(b2), col_stage, st);
   else
@@ -184,6 +236,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))
+#define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_mfma<HP_, BS_>))
+  AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
 #undef AFNO_ATTR
   return first;
 }

@@ -29,6 +29,8 @@ __device__ __forceinline__ void fill_roots(float2* tw) {
   }
 }
 
+// v * w^m (forward) or v * conj(w)^m (inverse).  The two-stage transforms pass m = j k2
+// with j < N1 and k2 < N2, so m < N1 N2 needs no reduction.
 template <bool INV>
 __device__ __forceinline__ float2 twiddle(float2 v, const float2* tw, int m) {
   float2 w = tw[m];
@@ -148,7 +150,7 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
     DftReg<N2, false>::run(v);
 #pragma unroll
     for (int k2 = 0; k2 < N2; ++k2)
-      F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<false>(v[k2], tw, (j * k2) % W);
+      F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<false>(v[k2], tw, j * k2);
   }
   __syncthreads();
   // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
@@ -271,7 +273,7 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
   DftReg<N2, true>::run(v);
 #pragma unroll
   for (int k2 = 0; k2 < N2; ++k2)
-    F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<true>(v[k2], tw, (j * k2) % W);
+    F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<true>(v[k2], tw, j * k2);
   __syncthreads();
   // ---- second stage: task (p, k2) -> y at w = k2 + N2 k1, held until F is free
   float2 yv[TP2][N1];
@@ -464,7 +466,10 @@ column_fast(T* __restrict__ S, const typename FragWord<T>::type* __restrict__ wf
   T* tile = reinterpret_cast<T*>(smem_raw);
   FT* F = reinterpret_cast<FT*>(smem_raw);
   float2* tw = reinterpret_cast<float2*>(reinterpret_cast<char*>(smem_raw) + L::kRegion);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is uniform across the wave: held in a scalar register, offsets derived
+  // from it can be buffer soffsets
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   const int blk = blockIdx.x % nb;  // consecutive workgroups -> different XCDs -> blocks
   const int rest = blockIdx.x / nb;
@@ -500,7 +505,7 @@ column_fast(T* __restrict__ S, const typename FragWord<T>::type* __restrict__ wf
 #pragma unroll
         for (int k2 = 0; k2 < N2; ++k2)
           st_f(F + ((k2 * N1 + j) * BS + c) * 2,
-               k2 == 0 ? va[u][0] : twiddle<false>(va[u][k2], tw, (j * k2) % H));
+               k2 == 0 ? va[u][0] : twiddle<false>(va[u][k2], tw, j * k2));
       }
     }
   }
@@ -617,7 +622,7 @@ column_fast(T* __restrict__ S, const typename FragWord<T>::type* __restrict__ wf
 #pragma unroll
         for (int k2 = 0; k2 < N2; ++k2)
           st_f(F + ((k2 * N1 + j) * BS + c) * 2,
-               k2 == 0 ? vc[u][0] : twiddle<true>(vc[u][k2], tw, (j * k2) % H));
+               k2 == 0 ? vc[u][0] : twiddle<true>(vc[u][k2], tw, j * k2));
       }
     }
   }

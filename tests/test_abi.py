@@ -118,4 +118,5 @@ def test_missing_library_raises(monkeypatch, tmp_path):
 def test_kernel_path_switch_validation():
     assert afno.afno_set_kernel_path(7) == afno.AFNO_ERR_INVALID_ARG
     assert afno.afno_set_kernel_path(afno.AFNO_PATH_GENERIC) == afno.AFNO_OK
+    assert afno.afno_set_kernel_path(afno.AFNO_PATH_VALU_DFT) == afno.AFNO_OK
     assert afno.afno_set_kernel_path(afno.AFNO_PATH_AUTO) == afno.AFNO_OK

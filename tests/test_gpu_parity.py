@@ -30,14 +30,26 @@ def _need_gpu():
 _PATH = {"now": "auto"}
 
 
-@pytest.fixture(params=["auto", "generic"])
+_PATHS = {"auto": afno.AFNO_PATH_AUTO, "valu": afno.AFNO_PATH_VALU_DFT,
+          "generic": afno.AFNO_PATH_GENERIC}
+
+
+@pytest.fixture(params=["auto", "valu", "generic"])
 def kernel_path(request):
-    """Run a test on the size-specialised kernels (auto) and on the size-generic ones."""
-    afno.set_kernel_path(afno.AFNO_PATH_GENERIC if request.param == "generic" else afno.AFNO_PATH_AUTO)
+    """Run a test on the default kernels (auto: bf16 columns with H <= 96 take the
+    matrix-core DFT kernel), on the same without that kernel (valu: vector-ALU FFT column
+    kernels) and on the size-generic kernels."""
+    afno.set_kernel_path(_PATHS[request.param])
     _PATH["now"] = request.param
     yield request.param
     afno.set_kernel_path(afno.AFNO_PATH_AUTO)
     _PATH["now"] = "auto"
+
+
+def _skip_same_as_auto(kernel_path, dtype, H, bs):
+    """valu differs from auto only where auto takes the matrix-core DFT column kernel."""
+    if kernel_path == "valu" and not (dtype == "bf16" and H <= 96 and bs in (32, 64, 96)):
+        pytest.skip("valu runs the same kernels as auto here")
 
 
 def _run(x_st, w_st, wl, stage=None, keep=None):
@@ -77,22 +89,26 @@ def _check_full(wl, x_st, w_st, label):
 
 def test_afno16x32_fp32_full(kernel_path):
     wl = synth.WORKLOADS["afno16x32_c64_nb4_fp32"]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
 def test_afno90x180_fp32_full(kernel_path):
     wl = synth.WORKLOADS["afno90x180_c768_nb8_fp32"]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
 def test_afno90x180_bf16_b4_full(kernel_path):
     wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), wl.name)
 
 
 def test_afno180x360_bf16_sampled_blocks(kernel_path):
     """Full 1 x 180 x 360 x 1024 call; the oracle recomputes blocks 0 and 7 alone."""
     wl = synth.WORKLOADS["afno180x360_c1024_nb8_bf16"]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
     say(f"[parity] {wl.name}: full GPU call, oracle on blocks 0 and 7")
     g = _run(x_st, w_st, wl)
@@ -131,6 +147,7 @@ def test_afno90x180_bf16_ensemble100_keep05_sampled_members(kernel_path):
 @pytest.mark.parametrize("name", ["afno16x32_c64_nb4_fp32", "afno90x180_c768_nb8_fp32"])
 def test_stage_spectra_fp32(name, kernel_path):
     wl = synth.WORKLOADS[name]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
     say(f"[stage] {name}")
     _, st = oracle_run(x_st, w_st, wl, stages=True)
@@ -178,6 +195,16 @@ EDGE = [
     (1, 90, 32, 192, 2, "fp32", 0.01, 0.8),
     (1, 16, 360, 96, 1, "bf16", 0.01, 0.5),
     (3, 16, 40, 64, 4, "bf16", 0.01, 1.0),
+    # bf16 columns on the matrix-core DFT kernel: padded heights 32 / 64 / 96 with block
+    # sizes 32 / 64 / 96, padding rows (H < HP), cutoffs, and the degenerate H = 1, 2
+    (1, 96, 24, 128, 2, "bf16", 0.01, 1.0),
+    (2, 50, 20, 192, 2, "bf16", 0.01, 0.8),
+    (1, 64, 16, 64, 2, "bf16", 0.02, 1.0),
+    (2, 27, 30, 128, 2, "bf16", 0.01, 1.0),
+    (1, 75, 12, 32, 1, "bf16", 0.01, 0.5),
+    (1, 60, 32, 128, 2, "bf16", 0.01, 1.0),
+    (2, 1, 4, 64, 2, "bf16", 0.01, 1.0),
+    (1, 2, 6, 32, 1, "bf16", 0.01, 1.0),
 ]
 
 
@@ -199,6 +226,7 @@ def _zero_weights(wl):
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_zero_weights_bit_exact_identity(dtype, kernel_path):
     wl = synth.Workload("zero", 2, 90, 180, 128, 2, dtype, 0.0, 1.0)
+    _skip_same_as_auto(kernel_path, dtype, wl.H, wl.bs)
     say(f"[edge] zero weights {dtype}")
     x_st = synth.make_x(wl)
     g = _run(x_st, _zero_weights(wl), wl)
@@ -208,6 +236,7 @@ def test_zero_weights_bit_exact_identity(dtype, kernel_path):
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_nothing_kept_bit_exact_identity(dtype, kernel_path):
     wl = synth.Workload("cut", 2, 16, 32, 64, 4, dtype, 0.01, 0.05)
+    _skip_same_as_auto(kernel_path, dtype, wl.H, wl.bs)
     say(f"[edge] nothing kept {dtype}")
     x_st = synth.make_x(wl)
     g = _run(x_st, synth.make_weights(wl), wl)
@@ -216,7 +245,28 @@ def test_nothing_kept_bit_exact_identity(dtype, kernel_path):
 
 def test_dc_only_cutoff(kernel_path):
     wl = synth.Workload("dc", 2, 16, 32, 64, 4, "fp32", 0.01, 0.115)
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
     _check_full(wl, synth.make_x(wl), synth.make_weights(wl), "DC-only cutoff")
+
+
+def test_matrix_core_and_valu_transforms_both_run():
+    """bf16, H = 90, bs = 96: the default path (matrix-core DFT column kernel) and
+    AFNO_PATH_VALU_DFT (vector-ALU FFT column kernel) both meet the bar and round
+    differently, so each really ran its own kernel."""
+    wl = synth.Workload("paths", 1, 90, 32, 192, 2, "bf16", 0.01, 1.0)
+    x_st, w_st = synth.make_x(wl, seed=9), synth.make_weights(wl, seed=9)
+    r = oracle_run(x_st, w_st, wl)
+    got = {}
+    try:
+        for name in ("auto", "valu"):
+            afno.set_kernel_path(_PATHS[name])
+            got[name] = _run(x_st, w_st, wl)
+            e = max_rel(got[name], r)
+            say(f"[paths] {name}: out rel {e:.3e}")
+            assert e <= TOL["bf16"]
+    finally:
+        afno.set_kernel_path(afno.AFNO_PATH_AUTO)
+    assert not np.array_equal(got["auto"], got["valu"])
 
 
 def test_batch_zero_is_noop():
@@ -228,6 +278,7 @@ def test_batch_zero_is_noop():
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_deterministic_bitwise(dtype, kernel_path):
     wl = synth.Workload("det", 2, 90, 180, 192, 2, dtype, 0.01, 1.0)
+    _skip_same_as_auto(kernel_path, dtype, wl.H, wl.bs)
     say(f"[edge] determinism {dtype}")
     x = to_dev(synth.make_x(wl), dtype)
     w = dev_weights(synth.make_weights(wl), dtype)
