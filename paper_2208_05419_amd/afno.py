@@ -29,7 +29,7 @@ AFNO_PATH_VALU_DFT = 2
 
 EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_profile_begin", "afno_profile_end",
             "afno_set_kernel_path", "afno_last_error", "afno_version")
-KERNELS = ("row_r2c", "column", "row_c2r")
+KERNELS = ("prep", "row_r2c", "column", "row_c2r")
 
 _ERR_NAMES = {AFNO_ERR_INVALID_ARG: "AFNO_ERR_INVALID_ARG", AFNO_ERR_UNSUPPORTED: "AFNO_ERR_UNSUPPORTED",
               AFNO_ERR_ALIAS: "AFNO_ERR_ALIAS", AFNO_ERR_HIP: "AFNO_ERR_HIP"}
@@ -124,7 +124,7 @@ def profile_begin(max_calls: int):
 
 def profile_end():
     """-> ({kernel name: summed ms}, timed calls)"""
-    ms = (ctypes.c_double * 3)()
+    ms = (ctypes.c_double * len(KERNELS))()
     calls = ctypes.c_int64()
     _check(afno_profile_end(ms, ctypes.byref(calls)))
     return dict(zip(KERNELS, list(ms))), int(calls.value)

@@ -164,14 +164,14 @@ struct Profile {
   std::mutex mu;
   bool on = false;
   int cap = 0, used = 0;
-  std::vector<hipEvent_t> ev;  // 4 per timed call
+  std::vector<hipEvent_t> ev;  // afno::kProfEvents per timed call
 };
 Profile g_prof;
 
 hipEvent_t* profile_slot() {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on || g_prof.used >= g_prof.cap) return nullptr;
-  return &g_prof.ev[4 * (size_t)g_prof.used++];
+  return &g_prof.ev[afno::kProfEvents * (size_t)g_prof.used++];
 }
 
 int run(const Args& a, int stage, float* dst, hipStream_t stream) {
@@ -248,7 +248,7 @@ int afno_profile_begin(int max_calls) {
   if (max_calls <= 0) return fail(AFNO_ERR_INVALID_ARG, "max_calls must be > 0");
   std::lock_guard<std::mutex> lk(g_prof.mu);
   for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
-  g_prof.ev.assign(4 * (size_t)max_calls, nullptr);
+  g_prof.ev.assign(afno::kProfEvents * (size_t)max_calls, nullptr);
   for (hipEvent_t& e : g_prof.ev) {
     hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) {
@@ -271,18 +271,18 @@ int afno_profile_end(double* kernel_ms, int64_t* calls) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on) return fail(AFNO_ERR_INVALID_ARG, "afno_profile_end without afno_profile_begin");
   int rc = AFNO_OK;
-  double sum[3] = {0.0, 0.0, 0.0};
+  double sum[afno::kProfEvents - 1] = {0.0, 0.0, 0.0, 0.0};
   for (int c = 0; c < g_prof.used && rc == AFNO_OK; ++c) {
-    hipEvent_t* ev = &g_prof.ev[4 * (size_t)c];
-    hipError_t r = hipEventSynchronize(ev[3]);
-    for (int k = 0; k < 3 && r == hipSuccess; ++k) {
+    hipEvent_t* ev = &g_prof.ev[afno::kProfEvents * (size_t)c];
+    hipError_t r = hipEventSynchronize(ev[afno::kProfEvents - 1]);
+    for (int k = 0; k < afno::kProfEvents - 1 && r == hipSuccess; ++k) {
       float ms = 0.f;
       r = hipEventElapsedTime(&ms, ev[k], ev[k + 1]);
       sum[k] += ms;
     }
     if (r != hipSuccess) rc = fail(AFNO_ERR_HIP, std::string("profile events: ") + hipGetErrorString(r));
   }
-  for (int k = 0; k < 3; ++k) kernel_ms[k] = sum[k];
+  for (int k = 0; k < afno::kProfEvents - 1; ++k) kernel_ms[k] = sum[k];
   *calls = g_prof.used;
   for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
   g_prof.ev.clear();

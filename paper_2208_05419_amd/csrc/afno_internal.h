@@ -16,6 +16,10 @@ constexpr int kColMaxMTiles = 12;     // 16-row MFMA tiles per column: H <= 192
 constexpr int kColMaxThreads = 512;   // 8 waves: bs <= 128
 constexpr int kLdsBytes = 160 * 1024; // LDS of one gfx950 CU
 
+// profile events per timed call: before the first kernel and after each of the four
+// phases (operand preparation, W forward, column, W inverse)
+constexpr int kProfEvents = 5;
+
 constexpr int kStageFull = 0;
 constexpr int kStageSpectrum = 1;
 constexpr int kStageMixed = 2;
@@ -63,7 +67,7 @@ bool use_mfma_col(const Plan& pl);  // under the current kernel path
 bool use_fast_col(const Plan& pl);  // under the current kernel path
 size_t frag_bytes(const Plan& pl);
 size_t mfma_tab_bytes(const Plan& pl);
-// ev: NULL, or 4 events recorded before the first kernel and after each of the three
+// ev: NULL, or kProfEvents events recorded before the first kernel and after each phase
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,
                          int stage, hipStream_t st, hipEvent_t* ev);

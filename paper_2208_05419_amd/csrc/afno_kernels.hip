@@ -90,16 +90,22 @@ static void launch_col_fast_one(const Plan& pl, T* S, const typename FragWord<T>
                      (int)pl.kept_h, pl.col.lam, pl.col.inv_sqrt_h, stage);
 }
 
-// Fragment-ordered weights first (into the workspace after the spectrum), then the column
-// kernel reads them with one load per fragment.
+// Fragment-ordered weights (into the workspace after the spectrum), read by the column
+// kernel with one load per fragment.
 template <typename T>
-static void launch_col_fast(const Plan& pl, T* S, const T* w1, const T* b1, const T* w2,
-                            const T* b2, int stage, hipStream_t st) {
+static void launch_prep_fast(const Plan& pl, void* S, const T* w1, const T* w2, hipStream_t st) {
   typedef typename FragWord<T>::type Word;
   Word* wf = reinterpret_cast<Word*>(reinterpret_cast<char*>(S) + pl.frag_offset);
   const int64_t words = pl.nb * frag_words_per_block<T>((int)pl.bs);
   const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
   hipLaunchKernelGGL(prep_weights<T>, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs, wf);
+}
+
+template <typename T>
+static void launch_col_fast(const Plan& pl, T* S, const T* b1, const T* b2, int stage,
+                            hipStream_t st) {
+  typedef typename FragWord<T>::type Word;
+  const Word* wf = reinterpret_cast<const Word*>(reinterpret_cast<const char*>(S) + pl.frag_offset);
   if (pl.H == 16 && pl.bs == 16)
     launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, wf, b1, b2, stage, st);
   else if (pl.H == 90 && pl.bs == 96)
@@ -122,17 +128,22 @@ size_t mfma_tab_bytes(const Plan& pl) {
   return (size_t)(2 * hp / 32) * (hp / 16) * 64 * 16;
 }
 
-// Fragment-ordered weights and the transform table into the workspace (one launch), then
-// the column kernel.
-static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* w1, const bf16* b1,
-                            const bf16* w2, const bf16* b2, int stage, hipStream_t st) {
+// Fragment-ordered weights and the transform table into the workspace, one launch.
+static void launch_prep_mfma(const Plan& pl, void* S, const bf16* w1, const bf16* w2,
+                             hipStream_t st) {
   uint4* wf = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.frag_offset);
   uint4* tab = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.tab_offset);
-  const int hp = mfma_col_hp(pl.H);
   const int64_t words = pl.nb * frag_words_per_block<bf16>((int)pl.bs) + (int64_t)(mfma_tab_bytes(pl) / 16);
   const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
   hipLaunchKernelGGL(prep_col_mfma, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs,
-                     (int)pl.H, hp, wf, tab);
+                     (int)pl.H, mfma_col_hp(pl.H), wf, tab);
+}
+
+static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* b1, const bf16* b2, int stage,
+                            hipStream_t st) {
+  const uint4* wf = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.frag_offset);
+  const uint4* tab = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.tab_offset);
+  const int hp = mfma_col_hp(pl.H);
   const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
 #define AFNO_CASE(HP_, BS_)                                                                 \
   if (hp == HP_ && pl.bs == BS_) {                                                          \
@@ -179,21 +190,30 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   const bool col_fast = use_fast_col(pl);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
   if (ev) (void)hipEventRecord(ev[0], st);
+  // prepared column-kernel operands (after the spectrum in the workspace; independent of x)
+  if (col_mfma) {
+    if constexpr (sizeof(T) == 2)  // mfma_col_available admits bf16 only
+      launch_prep_mfma(pl, S, static_cast<const bf16*>(w1), static_cast<const bf16*>(w2), st);
+  } else if (col_fast) {
+    launch_prep_fast<T>(pl, S, static_cast<const T*>(w1), static_cast<const T*>(w2), st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[1], st);
   if (row_fast)
     launch_row_fwd_fast<T>(pl, xt, St, st);
   else
     hipLaunchKernelGGL(row_r2c_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, xt, St, pl.row);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (ev) (void)hipEventRecord(ev[1], st);
+  if (ev) (void)hipEventRecord(ev[2], st);
   const int col_stage = (stage == kStageSpectrum) ? 1 : (stage == kStageMixed ? 2 : 0);
   if (col_mfma) {
-    if constexpr (sizeof(T) == 2)  // mfma_col_available admits bf16 only
-      launch_col_mfma(pl, St, static_cast<const bf16*>(w1), static_cast<const bf16*>(b1),
-                      static_cast<const bf16*>(w2), static_cast<const bf16*>(b2), col_stage, st);
+    if constexpr (sizeof(T) == 2)
+      launch_col_mfma(pl, St, static_cast<const bf16*>(b1), static_cast<const bf16*>(b2),
+                      col_stage, st);
   } else if (col_fast)
-    launch_col_fast<T>(pl, St, static_cast<const T*>(w1), static_cast<const T*>(b1),
-                       static_cast<const T*>(w2), static_cast<const T*>(b2), col_stage, st);
+    launch_col_fast<T>(pl, St, static_cast<const T*>(b1), static_cast<const T*>(b2), col_stage, st);
   else
     hipLaunchKernelGGL(column_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
                        dim3(pl.col_threads), pl.col_lds, st, St, static_cast<const T*>(w1),
@@ -201,7 +221,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
                        static_cast<const T*>(b2), pl.col, col_stage);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (ev) (void)hipEventRecord(ev[2], st);
+  if (ev) (void)hipEventRecord(ev[3], st);
   if (stage == kStageSpectrum || stage == kStageMixed) {
     const int64_t total = pl.B * pl.H * (pl.W / 2 + 1) * pl.C * 2;
     const unsigned g = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
@@ -216,7 +236,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
     hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, St, xt,
                        static_cast<T*>(out), dst, pl.row, mode);
   e = hipGetLastError();
-  if (ev && e == hipSuccess) (void)hipEventRecord(ev[3], st);
+  if (ev && e == hipSuccess) (void)hipEventRecord(ev[4], st);
   return e;
 }
 

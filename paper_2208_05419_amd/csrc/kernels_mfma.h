@@ -64,27 +64,27 @@ struct MfmaCol {
 
 // Transform table in fragment order: word (s * KT + t) * 64 + lane holds the B fragment of
 // k-step s and column tile t (lane: column 16 t + lane % 16, K rows 32 s + 8 (lane / 16) ...
-// + 7).  Entries rounded to bf16 from double precision.
+// + 7).  Entries rounded to bf16 from single precision.
 __device__ __forceinline__ uint4 dft_table_word(int64_t i, int H, int HP) {
   const int KT = HP / 16;
   const int lane = (int)(i & 63);
   const int64_t f = i >> 6;
   const int t = (int)(f % KT), s = (int)(f / KT);
   const int j = 16 * t + (lane & 15);
-  const double sc = 1.0 / sqrt((double)H);
+  const float sc = 1.0f / sqrtf((float)H);
   union { uint4 u; bf16 h[8]; } w;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int kap = 32 * s + 8 * (lane >> 4) + e;
     const int sigma = kap / HP, r = kap % HP;
-    double v = 0.0;
+    float v = 0.f;
     if (r < H && j < H) {
-      const int m = (int)(((int64_t)r * j) % H);
-      double sn, cs;
-      sincospi(2.0 * (double)m / (double)H, &sn, &cs);
+      const int m = (r * j) % H;  // the argument reduced exactly: 2 m / H in [0, 2)
+      float sn, cs;
+      sincospif(2.0f * (float)m / (float)H, &sn, &cs);
       v = sigma == 0 ? cs * sc : -sn * sc;
     }
-    w.h[e] = (bf16)(float)v;  // double -> float is exact to well below a bf16 ulp here
+    w.h[e] = (bf16)v;  // float is accurate far below the bf16 rounding step
   }
   return w.u;
 }
