@@ -37,6 +37,16 @@ namespace afno {
 // Column kernel, vector-ALU transforms: H = N1 N2 with block size BS.
 //   H = 16, BS = 16: 4 x 4;  H = 90, BS = 96: 9 x 10;  H = 180, BS = 128: 12 x 15 (bf16 only,
 //   with a bf16 transform intermediate: a float one would not fit the LDS).
+int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
+
+// words of the preparation job: the fragment-ordered weights, and the DFT table if with_tab
+static int64_t prep_words_host(const Plan& pl, bool with_tab) {
+  const int hp = mfma_col_hp(pl.H);
+  return pl.nb * (pl.dtype == 0 ? frag_words_per_block<float>((int)pl.bs)
+                                : frag_words_per_block<bf16>((int)pl.bs)) +
+         (with_tab ? (int64_t)(2 * hp / 32) * (hp / 16) * 64 : 0);
+}
+
 #define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
 bool fast_row_available(int64_t W, int64_t C) {
 #define AFNO_CASE(w, n1, n2, np) if (W == w) return C % (2 * np) == 0;
@@ -50,14 +60,19 @@ bool fast_col_available(int dtype, int64_t H, int64_t bs) {
   return dtype == 1 && H == 180 && bs == 128;
 }
 
+// pj.tout / pj.wout null: no preparation job; else its words go to extra workgroups
 template <typename T>
-static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, hipStream_t st) {
+static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, PrepJob<T> pj, hipStream_t st) {
   const unsigned gx = (unsigned)(pl.B * pl.H);
   const float sc = 0.5f * pl.row.inv_sqrt_w;
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
-    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(gx * (unsigned)(pl.C / (2 * np))), \
-                       dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc);            \
+    const unsigned nmain = gx * (unsigned)(pl.C / (2 * np));                              \
+    pj.nmain = (int)nmain;                                                                \
+    const unsigned nprep = pj.wout ? (unsigned)std::min<int64_t>(                         \
+        (prep_words_host(pl, pj.tout != nullptr) + np * n1 - 1) / (np * n1), 1024) : 0;   \
+    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nmain + nprep),              \
+                       dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc, pj);        \
     return;                                                                               \
   }
   AFNO_ROW_FAST_LIST(AFNO_CASE)
@@ -90,17 +105,6 @@ static void launch_col_fast_one(const Plan& pl, T* S, const typename FragWord<T>
                      (int)pl.kept_h, pl.col.lam, pl.col.inv_sqrt_h, stage);
 }
 
-// Fragment-ordered weights (into the workspace after the spectrum), read by the column
-// kernel with one load per fragment.
-template <typename T>
-static void launch_prep_fast(const Plan& pl, void* S, const T* w1, const T* w2, hipStream_t st) {
-  typedef typename FragWord<T>::type Word;
-  Word* wf = reinterpret_cast<Word*>(reinterpret_cast<char*>(S) + pl.frag_offset);
-  const int64_t words = pl.nb * frag_words_per_block<T>((int)pl.bs);
-  const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
-  hipLaunchKernelGGL(prep_weights<T>, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs, wf);
-}
-
 template <typename T>
 static void launch_col_fast(const Plan& pl, T* S, const T* b1, const T* b2, int stage,
                             hipStream_t st) {
@@ -117,8 +121,6 @@ static void launch_col_fast(const Plan& pl, T* S, const T* b1, const T* b2, int 
 #define AFNO_MFMA_COL_LIST(X) \
   X(32, 32) X(32, 64) X(32, 96) X(64, 32) X(64, 64) X(64, 96) X(96, 32) X(96, 64) X(96, 96)
 
-int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
-
 bool mfma_col_available(int dtype, int64_t H, int64_t bs) {
   return dtype == 1 && H <= 96 && (bs == 32 || bs == 64 || bs == 96);
 }
@@ -126,17 +128,6 @@ bool mfma_col_available(int dtype, int64_t H, int64_t bs) {
 size_t mfma_tab_bytes(const Plan& pl) {
   const int hp = mfma_col_hp(pl.H);
   return (size_t)(2 * hp / 32) * (hp / 16) * 64 * 16;
-}
-
-// Fragment-ordered weights and the transform table into the workspace, one launch.
-static void launch_prep_mfma(const Plan& pl, void* S, const bf16* w1, const bf16* w2,
-                             hipStream_t st) {
-  uint4* wf = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.frag_offset);
-  uint4* tab = reinterpret_cast<uint4*>(reinterpret_cast<char*>(S) + pl.tab_offset);
-  const int64_t words = pl.nb * frag_words_per_block<bf16>((int)pl.bs) + (int64_t)(mfma_tab_bytes(pl) / 16);
-  const unsigned g = (unsigned)std::min<int64_t>((words + 255) / 256, 4096);
-  hipLaunchKernelGGL(prep_col_mfma, dim3(g), dim3(256), 0, st, w1, w2, (int)pl.nb, (int)pl.bs,
-                     (int)pl.H, mfma_col_hp(pl.H), wf, tab);
 }
 
 static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* b1, const bf16* b2, int stage,
@@ -189,19 +180,23 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   const bool col_mfma = use_mfma_col(pl);
   const bool col_fast = use_fast_col(pl);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
+  // prepared column-kernel operands (after the spectrum in the workspace; independent of x):
+  // extra workgroups of the size-specialised W-axis forward launch, else a launch of their own
+  PrepJob<T> pj{static_cast<const T*>(w1), static_cast<const T*>(w2), nullptr, nullptr,
+                (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0};
+  if (col_mfma || col_fast)
+    pj.wout = reinterpret_cast<typename FragWord<T>::type*>(static_cast<char*>(S) + pl.frag_offset);
+  if (col_mfma) pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
   if (ev) (void)hipEventRecord(ev[0], st);
-  // prepared column-kernel operands (after the spectrum in the workspace; independent of x)
-  if (col_mfma) {
-    if constexpr (sizeof(T) == 2)  // mfma_col_available admits bf16 only
-      launch_prep_mfma(pl, S, static_cast<const bf16*>(w1), static_cast<const bf16*>(w2), st);
-  } else if (col_fast) {
-    launch_prep_fast<T>(pl, S, static_cast<const T*>(w1), static_cast<const T*>(w2), st);
+  if (pj.wout && !row_fast) {
+    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr) + 255) / 256, 4096);
+    hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], st);
   if (row_fast)
-    launch_row_fwd_fast<T>(pl, xt, St, st);
+    launch_row_fwd_fast<T>(pl, xt, St, pj, st);
   else
     hipLaunchKernelGGL(row_r2c_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, xt, St, pl.row);
   e = hipGetLastError();

@@ -16,6 +16,7 @@
 #include "afno_internal.h"
 #include "dft_reg.h"
 #include "kernel_common.h"
+#include "kernels_prep.h"
 
 namespace afno {
 
@@ -120,13 +121,20 @@ __device__ __forceinline__ float4 split_pair(float2 z, float2 zm, float s) {
 
 // ------------------------------------------------------------------ W-axis forward
 
-// grid B * H * C / (2 NP), block NP * N1.  NP complex signals (2 NP channels) per
-// workgroup; signal p of thread t = t % NP.
+// grid B * H * C / (2 NP) (= pj.nmain) + the workgroups of the appended preparation job,
+// block NP * N1.  NP complex signals (2 NP channels) per workgroup; signal p of thread
+// t = t % NP.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
-row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float scale) {
+row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float scale,
+             PrepJob<T> pj) {
   static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
   constexpr int NT = NP * N1;
+  if ((int)blockIdx.x >= pj.nmain) {  // appended workgroups: the column kernel's operands
+    prep_operands<T>((int64_t)(blockIdx.x - pj.nmain) * NT + threadIdx.x,
+                     (int64_t)(gridDim.x - pj.nmain) * NT, pj);
+    return;
+  }
   __shared__ float2 F[N2 * N1 * NP];
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
@@ -367,31 +375,6 @@ struct MlpGrid {
   static constexpr int NW = (2 * BS / 16) / WN;
   static_assert(WM * WN == kWaves && MW * WM == MT && NW * WN * 16 == 2 * BS, "MLP wave grid");
 };
-
-// Writes the fragment-ordered weights of both layers of every block (frag_words_per_block
-// words per block): each lane of the column kernel then fetches a whole B fragment with
-// one load at a wave-uniform offset, already permuted and sign-flipped.
-template <typename T>
-__global__ void __launch_bounds__(256)
-prep_weights(const T* __restrict__ w1, const T* __restrict__ w2, int nb, int bs,
-             typename FragWord<T>::type* __restrict__ out) {
-  const int nt16 = 2 * bs / 16, ksteps = 2 * bs / Mma<T>::kK;
-  const int64_t total = (int64_t)nb * frag_words_per_block<T>(bs);
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int lane = (int)(i & 63);
-    int64_t f = i >> 6;
-    const int t = (int)(f % nt16);
-    f /= nt16;
-    const int s = (int)(f % ksteps);
-    f /= ksteps;
-    const int layer = (int)(f & 1);
-    const int64_t blk = f >> 1;
-    const T* w = (layer ? w2 : w1) + blk * bs * bs * 2;
-    const int j = (16 * t + (lane & 15)) >> 1;
-    out[i] = FragWord<T>::make(w, bs, s * Mma<T>::kK, j, lane & 1, lane);
-  }
-}
 
 // One layer: acc[m][n] = (rows of the wave's m-tile m) x (real-ified complex weight of its
 // n-tile n), the weight fragments read from the prepared buffer wb (this block, this

@@ -30,6 +30,7 @@
 // [rho][c][k] planes for the inverse, Z^T goes to HBM as 8-byte (two channel) stores.
 #pragma once
 #include "kernel_common.h"
+#include "kernels_prep.h"
 
 namespace afno {
 
@@ -61,61 +62,6 @@ struct MfmaCol {
   static constexpr int kRegionBytes = ((kXBytes > kYBytes ? kXBytes : kYBytes) + 15) / 16 * 16;
   static constexpr int kBytes = kTabBytes + kRegionBytes;
 };
-
-// Transform table in fragment order: word (s * KT + t) * 64 + lane holds the B fragment of
-// k-step s and column tile t (lane: column 16 t + lane % 16, K rows 32 s + 8 (lane / 16) ...
-// + 7).  Entries rounded to bf16 from single precision.
-__device__ __forceinline__ uint4 dft_table_word(int64_t i, int H, int HP) {
-  const int KT = HP / 16;
-  const int lane = (int)(i & 63);
-  const int64_t f = i >> 6;
-  const int t = (int)(f % KT), s = (int)(f / KT);
-  const int j = 16 * t + (lane & 15);
-  const float sc = 1.0f / sqrtf((float)H);
-  union { uint4 u; bf16 h[8]; } w;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int kap = 32 * s + 8 * (lane >> 4) + e;
-    const int sigma = kap / HP, r = kap % HP;
-    float v = 0.f;
-    if (r < H && j < H) {
-      const int m = (r * j) % H;  // the argument reduced exactly: 2 m / H in [0, 2)
-      float sn, cs;
-      sincospif(2.0f * (float)m / (float)H, &sn, &cs);
-      v = sigma == 0 ? cs * sc : -sn * sc;
-    }
-    w.h[e] = (bf16)v;  // float is accurate far below the bf16 rounding step
-  }
-  return w.u;
-}
-
-// Prepared operands of the MFMA column kernel, one launch: the fragment-ordered block
-// weights (the layout the MLP products read) followed by the transform table.
-__global__ void __launch_bounds__(256)
-prep_col_mfma(const bf16* __restrict__ w1, const bf16* __restrict__ w2, int nb, int bs, int H,
-              int HP, uint4* __restrict__ wout, uint4* __restrict__ tout) {
-  const int nt16 = 2 * bs / 16, ksteps = 2 * bs / 32;
-  const int64_t nw = (int64_t)nb * frag_words_per_block<bf16>(bs);
-  const int64_t nt = (int64_t)(2 * HP / 32) * (HP / 16) * 64;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nw + nt;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    if (i >= nw) {
-      tout[i - nw] = dft_table_word(i - nw, H, HP);
-      continue;
-    }
-    const int lane = (int)(i & 63);
-    int64_t f = i >> 6;
-    const int t = (int)(f % nt16);
-    f /= nt16;
-    const int s = (int)(f % ksteps);
-    f /= ksteps;
-    const int layer = (int)(f & 1);
-    const int64_t blk = f >> 1;
-    const bf16* w = (layer ? w2 : w1) + blk * bs * bs * 2;
-    const int j = (16 * t + (lane & 15)) >> 1;
-    wout[i] = FragWord<bf16>::make(w, bs, s * 32, j, lane & 1, lane);
-  }
-}
 
 __device__ __forceinline__ bf16x8 as_frag(uint4 u) {
   union { uint4 u; bf16x8 f; } r;
@@ -177,7 +123,7 @@ __device__ __forceinline__ void dft_product(const bf16* P, const uint4* tab, int
 
 // grid B * KW * nb (block index fastest), 512 threads, dynamic LDS MfmaCol<HP, BS>::kBytes.
 // S: spectrum [B][H][KW][C] complex bf16, updated in place.  wfrag: fragment-ordered
-// weights (prep_col_mfma); dtab: transform table.  stage: 0 full, 1 stop after the
+// weights; dtab: transform table (both from prep_operands).  stage: 0 full, 1 stop after the
 // forward transform, 2 stop after the MLP (the column goes back to S as it is).
 template <int HP, int BS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
