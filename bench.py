@@ -5,10 +5,13 @@ A step is one full filter call (operand preparation, W-axis forward transform, c
 kernel with the H transforms and the block MLP, W-axis inverse transform + residual) on the
 90 x 180 x 768 bf16 workload with B = 4 (8 blocks of 96; synthetic N(0,1) fields
 scaled per channel by U(0.5, 2), complex weights N(0, 0.02^2), lambda 0.01, keep 1),
-with inputs resident in HBM.  value = samples per second = B / (time per step).
+with inputs resident in HBM.  value = samples per second = B / (time per step), measured
+after the GPU's clocks have settled (an untimed 0.3 s run of the filter before the W
+counted warm-up steps).
 
-Alongside: per-kernel HIP-event times on the launch stream over a second run of the same
-steps (the headline timing records no events between its steps),
+Alongside: the median, p10 and p90 of single calls (a second run of the same steps with
+one event between calls), per-kernel HIP-event times on the launch stream over a third run
+(the headline timing records no events between its steps),
 the roofline of the dominant kernel (algorithmic bytes or FLOPs per launch divided by
 its mean launch time), measured HBM traffic from stored rocprofv3 counters when they
 belong to the current kernel sources, the 100-member ensemble workload, and the float64
@@ -33,6 +36,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3       # fp32 matrix
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_afno90x180_c768_nb8_bf16_b4.json")
+PREWARM_S = 0.3                # untimed sustained run before the counted warm-up (clock ramp)
 # HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
 # sha256 of the kernel sources it was measured on (null once the kernels change)
 
@@ -90,6 +94,13 @@ def time_workload(wl, steps: int, warmup: int, seed: int = 0):
         afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep,
                             out=out, stream=stream)
 
+    # the GPU's clocks ramp up over tens of milliseconds of sustained work: run the filter for
+    # at least PREWARM_S seconds (untimed) before the counted warm-up steps
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < PREWARM_S:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -102,6 +113,16 @@ def time_workload(wl, steps: int, warmup: int, seed: int = 0):
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
+    # per-call distribution: the same steps again, one event between consecutive calls
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record(stream)
+    for i in range(steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per_call = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
+    pick = lambda q: per_call[min(steps - 1, int(q * steps))]  # noqa: E731
+    dist = {"median": round(pick(0.5), 5), "p10": round(pick(0.1), 5), "p90": round(pick(0.9), 5)}
     # the per-kernel breakdown: the same steps again with the library's per-phase events
     afno.profile_begin(steps)
     for _ in range(steps):
@@ -110,7 +131,7 @@ def time_workload(wl, steps: int, warmup: int, seed: int = 0):
     kernel_ms, calls = afno.profile_end()
     del x, w, out
     torch.cuda.empty_cache()
-    return total_ms / steps, {k: v / max(calls, 1) for k, v in kernel_ms.items()}, calls
+    return total_ms / steps, {k: v / max(calls, 1) for k, v in kernel_ms.items()}, calls, dist
 
 
 def roofline(wl, kern_ms: dict, es: int):
@@ -224,7 +245,7 @@ def main():
         calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[synth.HEADLINE]
     es = 2 if wl.dtype == "bf16" else 4
-    ms, kern_ms, calls = time_workload(wl, args.steps, args.warmup)
+    ms, kern_ms, calls, dist = time_workload(wl, args.steps, args.warmup)
     roof, per_kernel = roofline(wl, kern_ms, es)
     value = wl.B / (ms * 1e-3)
     line = {
@@ -245,14 +266,16 @@ def main():
         "roofline": roof,
         "kernels": per_kernel,
         "timed_calls": calls,
+        "call_ms": dist,
     }
     if not args.no_ensemble:
         ens = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
-        e_ms, e_kern, _ = time_workload(ens, max(args.steps // 5, 5), max(args.warmup // 5, 3))
+        e_ms, e_kern, _, e_dist = time_workload(ens, max(args.steps // 5, 5), max(args.warmup // 5, 3))
         e_roof, e_per = roofline(ens, e_kern, 2)
         e_roof["traffic"] = None
         line["ensemble"] = {"workload": ens.name, "samples_per_s": round(ens.B / (e_ms * 1e-3), 2),
-                            "ms_per_step": round(e_ms, 4), "kernels": e_per, "roofline": e_roof}
+                            "ms_per_step": round(e_ms, 4), "call_ms": e_dist, "kernels": e_per,
+                            "roofline": e_roof}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -158,8 +158,10 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
       const int c = task % BS, r0 = 8 * (task / BS);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        xv[u][e] = 0u;
-        if (task < XT && r0 + e < H) xv[u][e] = cb.ld32(c * 4u + (uint32_t)r0 * rsb, e * rsb);
+        // branch-free: rows outside the column load its first word and are zeroed
+        const bool ok = task < XT && r0 + e < H;
+        const uint32_t wv = cb.ld32(ok ? c * 4u + (uint32_t)(r0 + e) * rsb : 0u, 0);
+        xv[u][e] = ok ? wv : 0u;
       }
     }
     uint4 tv[TR];

@@ -54,6 +54,8 @@ WORKLOADS = {
         Workload("afno90x180_c768_nb8_bf16_b4", 4, 90, 180, 768, 8, "bf16", 0.01, 1.0,
                  "channel_scaled"),
         Workload("afno180x360_c1024_nb8_bf16", 1, 180, 360, 1024, 8, "bf16", 0.01, 1.0),
+        # the paper's own filter shape: 4x4 patches of the 0.25-degree grid, 32 blocks of 32
+        Workload("afno180x360_c1024_nb32_bf16", 1, 180, 360, 1024, 32, "bf16", 0.01, 1.0),
         Workload("afno90x180_c768_nb8_bf16_ens100_keep0.5", 100, 90, 180, 768, 8, "bf16", 0.01,
                  0.5, "ensemble"),
     ]

@@ -125,6 +125,27 @@ def test_afno180x360_bf16_sampled_blocks(kernel_path):
         assert e_out <= TOL["bf16"] and e_delta <= TOL["bf16"]
 
 
+def test_afno180x360_nb32_paper_shape_sampled_blocks(kernel_path):
+    """The paper's own filter shape (180 x 360 tokens, C = 1024 in 32 blocks of 32): full
+    call, the oracle recomputes blocks 0, 13 and 31 alone."""
+    wl = synth.WORKLOADS["afno180x360_c1024_nb32_bf16"]
+    _skip_same_as_auto(kernel_path, wl.dtype, wl.H, wl.bs)
+    x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
+    say(f"[parity] {wl.name}: full GPU call, oracle on blocks 0, 13, 31 (path {_PATH['now']})")
+    g = _run(x_st, w_st, wl)
+    gd = _run(x_st, w_st, wl, stage=afno.AFNO_STAGE_DELTA)
+    bs = wl.bs
+    for k in (0, 13, 31):
+        sl = slice(k * bs, (k + 1) * bs)
+        sub = synth.Workload(wl.name + f"_blk{k}", wl.B, wl.H, wl.W, bs, 1, wl.dtype, wl.lam, wl.keep)
+        r, st = oracle_run(np.ascontiguousarray(x_st[..., sl]),
+                           {n: np.ascontiguousarray(v[k:k + 1]) for n, v in w_st.items()}, sub,
+                           stages=True)
+        e_out, e_delta = max_rel(g[..., sl], r), max_rel(gd[..., sl], st["delta"])
+        say(f"  block {k}: out rel {e_out:.3e}  delta rel {e_delta:.3e}")
+        assert e_out <= TOL["bf16"] and e_delta <= TOL["bf16"]
+
+
 def test_afno90x180_bf16_ensemble100_keep05_sampled_members(kernel_path):
     """Full 100-member call with keep 0.5; the oracle recomputes members 0, 57 and 99."""
     wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
