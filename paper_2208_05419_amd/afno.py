@@ -51,6 +51,13 @@ def load_library():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"AFNO HIP library not built: {LIB_PATH} is missing "
                            "(run `python -c 'import __graft_entry__ as g; g.build()'`)")
+    # torch ships its own HIP runtime under the same soname; loading torch first makes the
+    # library bind to that runtime, so tensors torch allocated are valid device pointers here
+    # (loaded the other way round, the process would hold two runtimes)
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     i64, vp, f32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
     lib.afno_filter_forward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,

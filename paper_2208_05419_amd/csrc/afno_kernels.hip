@@ -35,8 +35,9 @@ namespace afno {
 // Column kernel, bf16 with H <= 96 and BS in {32, 64, 96}: H transforms as MFMA products
 //   against a transform table (kernels_mfma.h), H padded to HP in {32, 64, 96}.
 // Column kernel, vector-ALU transforms: H = N1 N2 with block size BS.
-//   H = 16, BS = 16: 4 x 4;  H = 90, BS = 96: 9 x 10;  H = 180, BS = 128: 12 x 15 (bf16 only,
-//   with a bf16 transform intermediate: a float one would not fit the LDS).
+//   H = 16, BS = 16: 4 x 4;  H = 90, BS = 96: 9 x 10;  H = 180, BS = 32: 12 x 15;
+//   H = 180, BS = 64 and 128: 12 x 15 (bf16 only, with a bf16 transform intermediate: a
+//   float one would not fit the LDS).
 int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
 
 // words of the preparation job: the fragment-ordered weights, and the DFT table if with_tab
@@ -56,8 +57,8 @@ bool fast_row_available(int64_t W, int64_t C) {
 }
 
 bool fast_col_available(int dtype, int64_t H, int64_t bs) {
-  if ((H == 16 && bs == 16) || (H == 90 && bs == 96)) return true;
-  return dtype == 1 && H == 180 && bs == 128;
+  if ((H == 16 && bs == 16) || (H == 90 && bs == 96) || (H == 180 && bs == 32)) return true;
+  return dtype == 1 && H == 180 && (bs == 64 || bs == 128);
 }
 
 // pj.tout / pj.wout null: no preparation job; else its words go to extra workgroups
@@ -114,8 +115,14 @@ static void launch_col_fast(const Plan& pl, T* S, const T* b1, const T* b2, int 
     launch_col_fast_one<T, float, 16, 4, 4, 16, 4>(pl, S, wf, b1, b2, stage, st);
   else if (pl.H == 90 && pl.bs == 96)
     launch_col_fast_one<T, float, 90, 9, 10, 96, 4, 512>(pl, S, wf, b1, b2, stage, st);
-  else if constexpr (sizeof(T) == 2)
-    launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, wf, b1, b2, stage, st);
+  else if (pl.H == 180 && pl.bs == 32)
+    launch_col_fast_one<T, float, 180, 12, 15, 32, 3, 256>(pl, S, wf, b1, b2, stage, st);
+  else if constexpr (sizeof(T) == 2) {
+    if (pl.bs == 64)
+      launch_col_fast_one<T, bf16, 180, 12, 15, 64, 3, 256>(pl, S, wf, b1, b2, stage, st);
+    else
+      launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, wf, b1, b2, stage, st);
+  }
 }
 
 #define AFNO_MFMA_COL_LIST(X) \
@@ -251,6 +258,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))
+  AFNO_ATTR((column_fast<float, float, 180, 12, 15, 32, 3, 256>))
+  AFNO_ATTR((column_fast<bf16, float, 180, 12, 15, 32, 3, 256>))
+  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 64, 3, 256>))
 #define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_mfma<HP_, BS_>))
   AFNO_MFMA_COL_LIST(AFNO_CASE)
 #undef AFNO_CASE
