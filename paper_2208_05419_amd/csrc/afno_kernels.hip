@@ -68,12 +68,12 @@ static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, PrepJob<T> pj,
   const float sc = 0.5f * pl.row.inv_sqrt_w;
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
-    const unsigned nmain = gx * (unsigned)(pl.C / (2 * np));                              \
+    const unsigned nmain = (unsigned)row_grid<np, (int)sizeof(T)>(gx, (int)(pl.C / (2 * np))); \
     pj.nmain = (int)nmain;                                                                \
     const unsigned nprep = pj.wout ? (unsigned)std::min<int64_t>(                         \
         (prep_words_host(pl, pj.tout != nullptr) + np * n1 - 1) / (np * n1), 1024) : 0;   \
     hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nmain + nprep),              \
-                       dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc, pj);        \
+                       dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc, (int64_t)gx, pj); \
     return;                                                                               \
   }
   AFNO_ROW_FAST_LIST(AFNO_CASE)
@@ -87,8 +87,9 @@ static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, 
   const float sc = pl.row.inv_sqrt_w;
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
-    hipLaunchKernelGGL((row_c2r_fast<T, w, n1, n2, np>), dim3(gx * (unsigned)(pl.C / (2 * np))), \
-                       dim3(np * n1), 0, st, S, x, out, dst, (int)pl.C, (int)pl.KW, sc, mode); \
+    const unsigned ng = (unsigned)row_grid<np, (int)sizeof(T)>(gx, (int)(pl.C / (2 * np))); \
+    hipLaunchKernelGGL((row_c2r_fast<T, w, n1, n2, np>), dim3(ng), dim3(np * n1), 0, st,  \
+                       S, x, out, dst, (int)pl.C, (int)pl.KW, sc, mode, (int64_t)gx);     \
     return;                                                                               \
   }
   AFNO_ROW_FAST_LIST(AFNO_CASE)

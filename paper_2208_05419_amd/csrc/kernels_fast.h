@@ -119,15 +119,47 @@ __device__ __forceinline__ float4 split_pair(float2 z, float2 zm, float s) {
   return make_float4((z.x + zm.x) * s, (z.y - zm.y) * s, (z.y + zm.y) * s, (zm.x - z.x) * s);
 }
 
+// ------------------------------------------------------------------ W-axis slices
+
+// Workgroup g -> (row b H + h, first channel c0) of a W-axis kernel over nrows rows of
+// nchunk slices of 2 NP channels.  A slice narrower than a 128-byte L2 line (bf16 with
+// 2 NP = 32 channels: 64 bytes per position) shares each line with the next slice, and
+// consecutive workgroups land on different XCDs, each with its own L2; so workgroups g and
+// g + 8, which the hardware deals to the same XCD (workgroups go to the 8 XCDs in turn),
+// take the two slices of one line, and each line is fetched into one L2 only.  That grid
+// is a multiple of 16 (row_grid); workgroups past the last slice pair get no slice.
+template <int NP, int ES>
+__host__ __device__ constexpr bool row_slices_paired(int nchunk) {
+  return 2 * NP * ES < 128 && nchunk % 2 == 0;
+}
+template <int NP, int ES>
+__host__ __device__ inline int64_t row_grid(int64_t nrows, int nchunk) {
+  return row_slices_paired<NP, ES>(nchunk) ? (nrows * nchunk + 15) / 16 * 16 : nrows * nchunk;
+}
+template <int NP, int ES>
+__device__ __forceinline__ bool row_slice(int g, int nchunk, int64_t nrows, int64_t& row, int& c0) {
+  if (row_slices_paired<NP, ES>(nchunk)) {
+    const int pairs = nchunk / 2;
+    const int64_t unit = (int64_t)(g >> 4) * 8 + (g & 7);
+    if (unit >= nrows * pairs) return false;
+    row = unit / pairs;
+    c0 = (int)(2 * (unit % pairs) + ((g >> 3) & 1)) * (2 * NP);
+    return true;
+  }
+  row = g / nchunk;
+  c0 = (g % nchunk) * (2 * NP);
+  return true;
+}
+
 // ------------------------------------------------------------------ W-axis forward
 
-// grid B * H * C / (2 NP) (= pj.nmain) + the workgroups of the appended preparation job,
-// block NP * N1.  NP complex signals (2 NP channels) per workgroup; signal p of thread
+// grid row_grid(B H, C / (2 NP)) (= pj.nmain) + the workgroups of the appended preparation
+// job, block NP * N1.  NP complex signals (2 NP channels) per workgroup; signal p of thread
 // t = t % NP.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
 row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float scale,
-             PrepJob<T> pj) {
+             int64_t nrows, PrepJob<T> pj) {
   static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
   constexpr int NT = NP * N1;
   if ((int)blockIdx.x >= pj.nmain) {  // appended workgroups: the column kernel's operands
@@ -138,10 +170,10 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
   __shared__ float2 F[N2 * N1 * NP];
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
-  // consecutive workgroups take consecutive channel chunks of one row (DRAM page locality)
-  const int nchunk = C / (2 * NP);
-  const int64_t row = blockIdx.x / nchunk;  // b * H + h
-  const int c0 = (int)(blockIdx.x % nchunk) * (2 * NP);
+  // the workgroup's row b H + h and channel slice
+  int64_t row;
+  int c0;
+  if (!row_slice<NP, (int)sizeof(T)>(blockIdx.x, C / (2 * NP), nrows, row, c0)) return;
   constexpr uint32_t es = sizeof(T);
   const uint32_t xrow = (uint32_t)C * es;        // bytes between consecutive w
   const uint32_t srow = (uint32_t)C * 2 * es;    // bytes between consecutive kw of S
@@ -161,45 +193,71 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
       F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<false>(v[k2], tw, j * k2);
   }
   __syncthreads();
-  // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
-  // for every k of both residue classes, so the two real spectra separate in registers.
-  constexpr int NPT = N2 / 2 + 1;
-  for (int task = tid; task < NP * NPT; task += NT) {
-    const int p = task % NP, q = task / NP;
-    const int qa = q, qb = (N2 - q) % N2;
-    float2 a[N1], b[N1];
+  if constexpr (N1 >= 24) {
+    // Long second-stage transforms: one task per (signal, residue class q), its N1-point
+    // DFT written back in place (slot (q, k1) of signal p then holds Z[q + N2 k1]), then the
+    // two real spectra separate from Z[k] and Z[W - k] with one task per (bin, signal), so
+    // every thread takes part in both steps.
+    for (int task = tid; task < NP * N2; task += NT) {
+      const int p = task % NP, q = task / NP;
+      float2 a[N1];
 #pragma unroll
-    for (int j = 0; j < N1; ++j) {
-      a[j] = F[(qa * N1 + j) * NP + p];
-      b[j] = F[(qb * N1 + j) * NP + p];
+      for (int j = 0; j < N1; ++j) a[j] = F[(q * N1 + j) * NP + p];
+      DftReg<N1, false>::run(a);
+#pragma unroll
+      for (int k1 = 0; k1 < N1; ++k1) F[(q * N1 + k1) * NP + p] = a[k1];
     }
-    DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
-    DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
-    const uint32_t va = 4 * p * es + qa * srow, vb = 4 * p * es + qb * srow;
+    __syncthreads();
+    const int nk = KW < W / 2 + 1 ? KW : W / 2 + 1;
+    for (int i = tid; i < nk * NP; i += NT) {
+      const int p = i % NP, k = i / NP;
+      const int km = k == 0 ? 0 : W - k;
+      const float2 z = F[((k % N2) * N1 + k / N2) * NP + p];
+      const float2 zm = F[((km % N2) * N1 + km / N2) * NP + p];
+      st_cpair(sb, (const T*)nullptr, 4 * p * es + k * srow, 0, split_pair(z, zm, scale));
+    }
+  } else {
+    // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
+    // for every k of both residue classes, so the two real spectra separate in registers.
+    constexpr int NPT = N2 / 2 + 1;
+    for (int task = tid; task < NP * NPT; task += NT) {
+      const int p = task % NP, q = task / NP;
+      const int qa = q, qb = (N2 - q) % N2;
+      float2 a[N1], b[N1];
 #pragma unroll
-    for (int k1 = 0; k1 < N1; ++k1) {
-      // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
-      const int ka = qa + N2 * k1;
-      const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
-      if (ka <= W / 2 && ka < KW)
-        st_cpair(sb, (const T*)nullptr, va, N2 * k1 * srow, split_pair(a[k1], zam, scale));
-      const int kb = qb + N2 * k1;
-      if (qb != qa && kb <= W / 2 && kb < KW)
-        st_cpair(sb, (const T*)nullptr, vb, N2 * k1 * srow, split_pair(b[k1], a[N1 - 1 - k1], scale));
+      for (int j = 0; j < N1; ++j) {
+        a[j] = F[(qa * N1 + j) * NP + p];
+        b[j] = F[(qb * N1 + j) * NP + p];
+      }
+      DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
+      DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
+      const uint32_t va = 4 * p * es + qa * srow, vb = 4 * p * es + qb * srow;
+#pragma unroll
+      for (int k1 = 0; k1 < N1; ++k1) {
+        // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
+        const int ka = qa + N2 * k1;
+        const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
+        if (ka <= W / 2 && ka < KW)
+          st_cpair(sb, (const T*)nullptr, va, N2 * k1 * srow, split_pair(a[k1], zam, scale));
+        const int kb = qb + N2 * k1;
+        if (qb != qa && kb <= W / 2 && kb < KW)
+          st_cpair(sb, (const T*)nullptr, vb, N2 * k1 * srow, split_pair(b[k1], a[N1 - 1 - k1], scale));
+      }
     }
   }
 }
 
 // ------------------------------------------------------------------ W-axis inverse + residual
 
-// grid B * H * C / (2 NP), block NP * N1.  mode 0: out = x + y (dtype T); mode 1: dst = y.
+// grid row_grid(B H, C / (2 NP)), block NP * N1.  mode 0: out = x + y (dtype T); mode 1:
+// dst = y.
 // Global traffic goes through LDS in 16-byte vectors: the kept half spectrum of the
 // workgroup's 2 NP channels is staged once (each stored bin feeds both Z[k] and Z[W-k]),
 // the residual is prefetched at kernel start, and the output leaves in 16-byte stores.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
 row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ out,
-             float* __restrict__ dst, int C, int KW, float scale, int mode) {
+             float* __restrict__ dst, int C, int KW, float scale, int mode, int64_t nrows) {
   static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
   constexpr int NT = NP * N1;
   constexpr int HALF = W / 2;
@@ -213,9 +271,9 @@ row_c2r_fast(const T* __restrict__ S, const T* __restrict__ x, T* __restrict__ o
   __shared__ float2 F[FN];                             // staged spectrum / stage-1 output / y
   __shared__ float2 tw[W];
   const int tid = threadIdx.x;
-  const int nchunk = C / (2 * NP);
-  const int64_t row = blockIdx.x / nchunk;
-  const int c0 = (int)(blockIdx.x % nchunk) * (2 * NP);
+  int64_t row;
+  int c0;
+  if (!row_slice<NP, (int)sizeof(T)>(blockIdx.x, C / (2 * NP), nrows, row, c0)) return;
   const uint32_t xrow = (uint32_t)C * es;
   const uint32_t srow = (uint32_t)C * 2 * es;
   const int64_t xbase = row * (int64_t)W * C + c0;
