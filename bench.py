@@ -14,10 +14,12 @@ one event between calls), per-kernel HIP-event times on the launch stream over a
 (the headline timing records no events between its steps),
 the roofline of the dominant kernel (algorithmic bytes or FLOPs per launch divided by
 its mean launch time), measured HBM traffic from stored rocprofv3 counters when they
-belong to the current kernel sources, the 100-member ensemble workload, and the float64
-CPU oracle timed on a bounded sample on the host cores.
+belong to the current kernel sources, the 100-member ensemble workload, the other
+workloads' throughput, and the float64 CPU oracle timed on a bounded sample on the host
+cores.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-ensemble] [--no-cpu-baseline]
+                    [--no-others]
 """
 from __future__ import annotations
 
@@ -37,6 +39,10 @@ BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3       # fp32 matrix
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_afno90x180_c768_nb8_bf16_b4.json")
 PREWARM_S = 0.3                # untimed sustained run before the counted warm-up (clock ramp)
+# timed after the headline for context: fp32 at the headline grid, the 180 x 360 grid with 8
+# blocks of 128, and the paper's own 180 x 360 filter with 32 blocks of 32
+OTHER_WORKLOADS = ("afno90x180_c768_nb8_fp32", "afno180x360_c1024_nb8_bf16",
+                   "afno180x360_c1024_nb32_bf16")
 # HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
 # sha256 of the kernel sources it was measured on (null once the kernels change)
 
@@ -224,6 +230,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-ensemble", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-others", action="store_true", help="skip the other workloads' timings")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="run one plain copy of this many MiB first (for counter scaling)")
@@ -276,6 +283,17 @@ def main():
         line["ensemble"] = {"workload": ens.name, "samples_per_s": round(ens.B / (e_ms * 1e-3), 2),
                             "ms_per_step": round(e_ms, 4), "call_ms": e_dist, "kernels": e_per,
                             "roofline": e_roof}
+    if not args.no_others:
+        # the remaining workloads: samples/s and per-kernel times (context; not the headline)
+        others = {}
+        for name in OTHER_WORKLOADS:
+            o = synth.WORKLOADS[name]
+            o_es = 2 if o.dtype == "bf16" else 4
+            o_ms, o_kern, _, _ = time_workload(o, max(args.steps // 5, 10), max(args.warmup // 5, 3))
+            _, o_per = roofline(o, o_kern, o_es)
+            others[name] = {"samples_per_s": round(o.B / (o_ms * 1e-3), 2), "ms_per_step": round(o_ms, 4),
+                            "kernel_ms": {k: v["ms"] for k, v in o_per.items()}}
+        line["other_workloads"] = others
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
