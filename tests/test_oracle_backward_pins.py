@@ -1,0 +1,142 @@
+"""Pins of the float64 backward oracle (oracle/backward.py) against things other than itself:
+central finite differences of the forward oracle (directional derivatives of
+L = <gout, out>), an independent float64 implementation differentiated by torch autograd
+(torch.fft's pocketfft transforms, which the forward pins tie to the same conventions), and
+the linear-regime closed form.  CPU only."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import backward as ob
+
+torch = pytest.importorskip("torch")
+
+
+def _rand(rng, *shape, s=1.0):
+    return rng.standard_normal(shape) * s
+
+
+def _case(seed, B=1, H=4, W=8, C=8, nb=2, wscale=0.3):
+    rng = np.random.default_rng(seed)
+    bs = C // nb
+    x = _rand(rng, B, H, W, C)
+    w = {"w1": _rand(rng, nb, bs, bs, 2, s=wscale), "b1": _rand(rng, nb, bs, 2, s=wscale),
+         "w2": _rand(rng, nb, bs, bs, 2, s=wscale), "b2": _rand(rng, nb, bs, 2, s=wscale)}
+    g = _rand(rng, B, H, W, C)
+    return x, w, g
+
+
+def _loss(x, w, g, nb, lam, keep):
+    out = oracle.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, lam, keep)
+    return float(np.sum(g * out))
+
+
+@pytest.mark.parametrize("seed,keep", [(0, 1.0), (1, 0.6), (2, 1.0)])
+def test_directional_derivatives_match_finite_differences(seed, keep):
+    """<grad, e> = (L(p + eps e) - L(p - eps e)) / (2 eps) for random directions e of every
+    input; the random point sits away from the ReLU and softshrink kinks."""
+    nb, lam = 2, 0.05
+    x, w, g = _case(seed)
+    # lam and keep as the float32 values the ABI passes
+    lam32, keep32 = float(np.float32(lam)), float(np.float32(keep))
+    grads = ob.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], g, nb, lam32, keep32)
+    rng = np.random.default_rng(100 + seed)
+    eps = 1e-6
+    for name in ("x", "w1", "b1", "w2", "b2"):
+        for _ in range(2):
+            base = x if name == "x" else w[name]
+            e = rng.standard_normal(base.shape)
+
+            def at(t):
+                if name == "x":
+                    return _loss(x + t * e, w, g, nb, lam32, keep32)
+                w2_ = dict(w)
+                w2_[name] = w[name] + t * e
+                return _loss(x, w2_, g, nb, lam32, keep32)
+
+            fd = (at(eps) - at(-eps)) / (2 * eps)
+            an = float(np.sum(grads["d" + name] * e))
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def _torch_forward(x, w, nb, lam, keep):
+    """Independent float64 forward: torch.fft (pocketfft) transforms, complex matmuls, the
+    cutoff recomputed from its definition (per-axis low |frequency| counts, floor in double)."""
+    B, H, W, C = x.shape
+    bs = C // nb
+    Wm = W // 2 + 1
+    cw = lambda a: torch.complex(a[..., 0], a[..., 1])  # noqa: E731
+    X = torch.fft.rfft2(x, dim=(1, 2), norm="ortho").reshape(B, H, Wm, nb, bs)
+    v = torch.einsum("bhwki,kij->bhwkj", X, cw(w["w1"])) + cw(w["b1"])
+    h = torch.complex(torch.relu(v.real), torch.relu(v.imag))
+    o = torch.einsum("bhwkj,kjl->bhwkl", h, cw(w["w2"])) + cw(w["b2"])
+    z = torch.complex(torch.nn.functional.softshrink(o.real, lam), torch.nn.functional.softshrink(o.imag, lam))
+    kept_h = int(np.floor((H // 2 + 1) * keep))
+    kept_w = int(np.floor(Wm * keep))
+    rows = torch.tensor([abs(r if r <= H // 2 else r - H) < kept_h for r in range(H)])
+    cols = torch.arange(Wm) < kept_w
+    mask = (rows[:, None] & cols[None, :]) if kept_h > 0 else torch.zeros(H, Wm, dtype=torch.bool)
+    z = z * mask[None, :, :, None, None]
+    y = torch.fft.irfft2(z.reshape(B, H, Wm, C), s=(H, W), dim=(1, 2), norm="ortho")
+    return x + y
+
+
+@pytest.mark.parametrize("shape,keep", [((2, 6, 10, 12, 3), 1.0), ((1, 9, 12, 16, 2), 0.7),
+                                        ((1, 5, 6, 8, 1), 1.0)])
+def test_matches_autograd_of_independent_forward(shape, keep):
+    B, H, W, C, nb = shape
+    lam = float(np.float32(0.05))
+    keep = float(np.float32(keep))
+    x, w, g = _case(7, B, H, W, C, nb)
+    grads = ob.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], g, nb, lam, keep)
+    xt = torch.tensor(x, requires_grad=True)
+    wt = {k: torch.tensor(v, requires_grad=True) for k, v in w.items()}
+    out = _torch_forward(xt, wt, nb, lam, keep)
+    # the independent forward agrees with the forward oracle first
+    ref = oracle.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, lam, keep)
+    assert np.max(np.abs(out.detach().numpy() - ref)) < 1e-12
+    (out * torch.tensor(g)).sum().backward()
+    for name, t in (("dx", xt), ("dw1", wt["w1"]), ("db1", wt["b1"]), ("dw2", wt["w2"]), ("db2", wt["b2"])):
+        a, b = grads[name], t.grad.numpy()
+        assert np.max(np.abs(a - b)) <= 1e-10 * max(1.0, np.max(np.abs(b))), name
+
+
+def test_linear_regime_closed_form():
+    """w1 = a I, b1 = beta (1 + i) with beta large (ReLU never clips), w2 = I,
+    b2 = -beta (1 + i), lam = 0, everything kept: out = (1 + a) x, so dx = (1 + a) g; and
+    the layer-2 input h = X a + beta (1 + i) makes dW2 = sum conj(h)^T do with do = dz."""
+    B, H, W, C, nb = 1, 6, 8, 8, 2
+    bs = C // nb
+    a, beta = 0.37, 100.0
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((B, H, W, C))
+    g = rng.standard_normal((B, H, W, C))
+    eye = np.zeros((nb, bs, bs, 2))
+    eye[..., 0] = np.eye(bs)
+    w1 = a * eye
+    w2 = eye.copy()
+    b1 = np.zeros((nb, bs, 2)) + beta
+    b2 = np.zeros((nb, bs, 2)) - beta
+    grads = ob.filter_backward(x, w1, b1, w2, b2, g, nb, 0.0, 1.0)
+    assert np.max(np.abs(grads["dx"] - (1 + a) * g)) < 1e-9
+    # db2 = sum over modes of dz = c_kw F(g) summed over modes (complex), per channel
+    c = ob.c_weights(W)
+    dz = (c[None, None, :, None] * oracle.rfft2(g)).sum(axis=(0, 1, 2)).reshape(nb, bs)
+    assert np.max(np.abs(grads["db2"][..., 0] - dz.real)) < 1e-9
+    assert np.max(np.abs(grads["db2"][..., 1] - dz.imag)) < 1e-9
+
+
+def test_inactive_softshrink_gives_pass_through_gradient():
+    """Zero weights and |b2| < lam everywhere: the filter output is identically 0 near this
+    point, so dx = g and every weight and bias gradient is 0."""
+    B, H, W, C, nb = 1, 4, 6, 8, 2
+    bs = C // nb
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((B, H, W, C))
+    g = rng.standard_normal((B, H, W, C))
+    z = np.zeros((nb, bs, bs, 2))
+    b2 = np.full((nb, bs, 2), 0.01)
+    grads = ob.filter_backward(x, z, np.zeros((nb, bs, 2)), z, b2, g, nb, 0.05, 1.0)
+    assert np.array_equal(grads["dx"], g)
+    for k in ("dw1", "db1", "dw2", "db2"):
+        assert not np.any(grads[k])
