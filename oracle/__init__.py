@@ -96,8 +96,10 @@ def keep_mask(H: int, W: int, keep: float) -> np.ndarray:
                      for a in range(H)])
 
 
-def rfft2(x) -> np.ndarray:
-    """Forward spectrum [B,H,Wm,C] complex128 of real x [B,H,W,C] (direct DFT, W then H)."""
+def rfft2(x, mid=None) -> np.ndarray:
+    """Forward spectrum [B,H,Wm,C] complex128 of real x [B,H,W,C] (direct DFT, W then H).
+    mid, if given, maps the W-axis spectrum [B,H,Wm,C,2] (re, im) before the H-axis DFT (a
+    storage rounding between the two passes)."""
     x = _f64(x)
     B, H, W, C = x.shape
     Wm = W // 2 + 1
@@ -105,6 +107,8 @@ def rfft2(x) -> np.ndarray:
     s2 = np.empty_like(s1)
     lib = _load()
     _check(lib.orc_dft_w_r2c(_ptr(x), B, H, W, C, _ptr(s1)), "dft_w_r2c")
+    if mid is not None:
+        s1 = _f64(mid(s1))
     _check(lib.orc_dft_h(_ptr(s1), B, H, Wm, C, -1, _ptr(s2)), "dft_h")
     return s2[..., 0] + 1j * s2[..., 1]
 

@@ -35,7 +35,7 @@ weight gradient is returned as (d/dre, d/dim) pairs in the weights' own layout
 [nb][in][out][2]; for v = X W, d/dW_re + i d/dW_im = conj(X) dv.
 
 The transforms are the forward oracle's (direct DFTs); the block products are plain complex
-einsums in float64.
+batched matrix products in float64.
 """
 from __future__ import annotations
 
@@ -62,9 +62,56 @@ def _pairs(z: np.ndarray) -> np.ndarray:
     return np.stack([z.real, z.imag], axis=-1)
 
 
-def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: float):
+def _blocks(A, Wk):
+    """Per-block product: A [..., nb, i] times Wk [nb, i, j] -> [..., nb, j] (a batched matmul)."""
+    lead = A.shape[:-2]
+    nb, ni = A.shape[-2:]
+    a = A.reshape(-1, nb, ni).transpose(1, 0, 2)
+    return np.matmul(a, Wk).transpose(1, 0, 2).reshape(*lead, nb, Wk.shape[-1])
+
+
+def _gram(A, Bm):
+    """sum over modes of A^T B per block: A [..., nb, i], B [..., nb, j] -> [nb, i, j]."""
+    nb = A.shape[-2]
+    a = A.reshape(-1, nb, A.shape[-1]).transpose(1, 2, 0)
+    b = Bm.reshape(-1, nb, Bm.shape[-1]).transpose(1, 0, 2)
+    return np.matmul(a, b)
+
+
+def round_bf16(a) -> np.ndarray:
+    """Nearest bfloat16 value (ties to even) of each float64, through float32 (the value a
+    float32 computation stores as bf16)."""
+    f = np.ascontiguousarray(np.asarray(a, dtype=np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32).astype(np.float64)
+    return np.where(np.isfinite(f), out, f.astype(np.float64))
+
+
+def _round_c(z, rnd):
+    return rnd(z.real) + 1j * rnd(z.imag)
+
+
+def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: float,
+                    band: float = 0.0, decide: str = "exact"):
     """Gradients of L with dL/dout = gout: returns dict dx [B,H,W,C], dw1, dw2 [nb,bs,bs,2],
-    db1, db2 [nb,bs,2], all float64."""
+    db1, db2 [nb,bs,2], all float64.
+
+    band > 0 adds the kink allowance: the gradients are step functions of the pre-activations
+    at relu's kink (v = 0) and the softshrink's (|o| = lam), so an implementation whose v or o
+    differ from the exact ones by up to band * rms(v) (band * rms(o)) may take either branch
+    for elements that close to a kink.  allow_<name> bounds, elementwise, how far its gradient
+    can move when any set of those ambiguous branches flips (first order: each flip taken
+    alone, their magnitudes summed; a flip at one kink does not move another), and n_kinks
+    counts the ambiguous elements (v, o).
+
+    decide selects the precision of the two mask decisions (relu's v > 0, the softshrink's
+    |o| > lam); the gradient values are float64 either way.  "exact": v and o in float64.
+    "bf16": v and o from bf16-stored intermediates, as a bf16-storage implementation forms
+    them: the W-axis spectrum, the 2-D spectrum X and the hidden layer h rounded to bf16
+    (products and sums then exact).  Near a kink a bf16 implementation decides on those
+    rounded operands; the decision itself is a step, so the comparison takes it in the
+    implementation's precision."""
     x = _f64(x)
     g = _f64(gout)
     B, H, W, C = x.shape
@@ -80,21 +127,64 @@ def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: 
 
     # forward state, block by block
     X = rfft2(x).reshape(B, H, Wm, nb, bs)
-    v = np.einsum("bhwki,kij->bhwkj", X, W1) + B1
+    v = _blocks(X, W1) + B1
     h = np.maximum(v.real, 0.0) + 1j * np.maximum(v.imag, 0.0)
-    o = np.einsum("bhwkj,kjl->bhwkl", h, W2) + B2
+    o = _blocks(h, W2) + B2
     kept = keep_mask(H, W, keep)[None, :, :, None, None]
+    if decide == "exact":
+        v_dec, o_dec = v, o
+    elif decide == "bf16":
+        Xr = _round_c(rfft2(x, mid=round_bf16), round_bf16).reshape(B, H, Wm, nb, bs)
+        v_dec = _blocks(Xr, W1) + B1
+        hr = _round_c(np.maximum(v_dec.real, 0.0) + 1j * np.maximum(v_dec.imag, 0.0), round_bf16)
+        o_dec = _blocks(hr, W2) + B2
+    else:
+        raise ValueError(f"unknown decide {decide!r}")
 
     # backward
     dz = (c[None, None, :, None] * rfft2(g)).reshape(B, H, Wm, nb, bs)
-    do = (dz.real * (np.abs(o.real) > lam) + 1j * dz.imag * (np.abs(o.imag) > lam)) * kept
-    dh = np.einsum("bhwkl,kjl->bhwkj", do, np.conj(W2))
-    dv = dh.real * (v.real > 0) + 1j * dh.imag * (v.imag > 0)
-    dX = np.einsum("bhwkj,kij->bhwki", dv, np.conj(W1))
-    dw2 = np.einsum("bhwkj,bhwkl->kjl", np.conj(h), do)
-    dw1 = np.einsum("bhwki,bhwkj->kij", np.conj(X), dv)
+    do = (dz.real * (np.abs(o_dec.real) > lam) + 1j * dz.imag * (np.abs(o_dec.imag) > lam)) * kept
+    dh = _blocks(do, np.conj(W2).transpose(0, 2, 1))
+    dv = dh.real * (v_dec.real > 0) + 1j * dh.imag * (v_dec.imag > 0)
+    dX = _blocks(dv, np.conj(W1).transpose(0, 2, 1))
+    dw2 = _gram(np.conj(h), do)
+    dw1 = _gram(np.conj(X), dv)
     db2 = do.sum(axis=(0, 1, 2))
     db1 = dv.sum(axis=(0, 1, 2))
     dx = g + irfft2(dX.reshape(B, H, Wm, C) / c[None, None, :, None], W)
-    return {"dx": dx, "dw1": _pairs(dw1), "db1": _pairs(db1), "dw2": _pairs(dw2),
-            "db2": _pairs(db2)}
+    res = {"dx": dx, "dw1": _pairs(dw1), "db1": _pairs(db1), "dw2": _pairs(dw2),
+           "db2": _pairs(db2)}
+    if band > 0.0:
+        res.update(_kink_allowance(X, v_dec, h, o_dec, dz, dh, kept, W1, W2, lam, band, H * W))
+    return res
+
+
+def _kink_allowance(X, v, h, o, dz, dh, kept, W1, W2, lam, band, hw):
+    """Elementwise bounds on the gradient change from flipping ambiguous mask entries (see
+    filter_backward).  A relu flip at (mode, block, j, part) moves dv_j by the part's dh value a:
+    dW1[:, j] by |X_i| a, db1[j] by a, dX_i by a |W1_ij|.  A softshrink flip at (..., l, part)
+    moves do_l by the part's dz value a: db2[l] by a, dW2[:, l] by |h_j| a, dh_j by at most
+    e_j = a |W2_jl|, and so dv_j, db1[j] by e_j, dW1[:, j] by |X_i| e_j, dX_i by sum_j e_j |W1_ij|.
+    dX at one mode reaches every pixel of its sample through the half-spectrum inverse with at
+    most |dX| / sqrt(H W)."""
+    rms_v = np.sqrt(np.mean(v.real ** 2 + v.imag ** 2) / 2)
+    rms_o = np.sqrt(np.mean(o.real ** 2 + o.imag ** 2) / 2)
+    a1r = np.abs(dh.real) * (np.abs(v.real) <= band * rms_v)
+    a1i = np.abs(dh.imag) * (np.abs(v.imag) <= band * rms_v)
+    near = lambda t: np.abs(np.abs(t) - lam) <= band * rms_o  # noqa: E731
+    a2r = np.abs(dz.real) * near(o.real) * kept
+    a2i = np.abs(dz.imag) * near(o.imag) * kept
+    s1, s2 = a1r + a1i, a2r + a2i                            # [B, H, Wm, nb, bs]
+    e = _blocks(s2, np.abs(W2).transpose(0, 2, 1))           # e_j = sum_l s2_l |W2_jl|
+    both = lambda t: np.stack([t, t], axis=-1)  # noqa: E731
+    dw1 = _gram(np.abs(X), s1 + e)
+    dw2 = _gram(np.abs(h), s2)
+    db1 = np.stack([(a1r + e).sum(axis=(0, 1, 2)), (a1i + e).sum(axis=(0, 1, 2))], axis=-1)
+    db2 = np.stack([a2r.sum(axis=(0, 1, 2)), a2i.sum(axis=(0, 1, 2))], axis=-1)
+    dX = _blocks(s1 + e, np.abs(W1).transpose(0, 2, 1))     # [B, H, Wm, nb, bs]
+    B = X.shape[0]
+    per_sample = dX.reshape(B, -1, dX.shape[-2] * dX.shape[-1]).sum(axis=1) / np.sqrt(hw)
+    n = int(np.count_nonzero(a1r) + np.count_nonzero(a1i) + np.count_nonzero(a2r) +
+            np.count_nonzero(a2i))
+    return {"allow_dx": per_sample[:, None, None, :], "allow_dw1": both(dw1),
+            "allow_db1": db1, "allow_dw2": both(dw2), "allow_db2": db2, "n_kinks": n}

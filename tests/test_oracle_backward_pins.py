@@ -140,3 +140,43 @@ def test_inactive_softshrink_gives_pass_through_gradient():
     assert np.array_equal(grads["dx"], g)
     for k in ("dw1", "db1", "dw2", "db2"):
         assert not np.any(grads[k])
+
+
+def test_round_bf16_matches_the_stored_form():
+    """round_bf16 agrees with the input generator's float32 -> bf16 bits (an independent
+    routine), ties and specials included."""
+    from paper_2208_05419_amd import synth
+    rng = np.random.default_rng(7)
+    f = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-6, 6, 4000),
+                        np.array([0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9,
+                                  -(1.0 + 2 ** -8), 3.0e38])]).astype(np.float32)
+    want = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(f)).astype(np.float64)
+    assert np.array_equal(ob.round_bf16(f.astype(np.float64)), want)
+    assert ob.round_bf16(np.array([1.0 + 2 ** -8]))[0] == 1.0          # tie to even
+    assert ob.round_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+def test_kink_allowance_bounds_decision_flips():
+    """Taking the mask decisions from bf16-rounded operands flips some of them; every such
+    gradient difference lies within the exact-decision allowance of a band wide enough to hold
+    the rounding (flips are planted by the bf16 decisions, values stay float64).  With band 0
+    the allowance is absent."""
+    rng = np.random.default_rng(11)
+    B, H, W, C, nb, lam = 2, 6, 10, 32, 2, 0.02
+    bs = C // nb
+    x = rng.standard_normal((B, H, W, C))
+    w = {"w1": rng.standard_normal((nb, bs, bs, 2)) * 0.2, "b1": rng.standard_normal((nb, bs, 2)) * 0.02,
+         "w2": rng.standard_normal((nb, bs, bs, 2)) * 0.2, "b2": rng.standard_normal((nb, bs, 2)) * 0.02}
+    g = rng.standard_normal(x.shape)
+    args = (x, w["w1"], w["b1"], w["w2"], w["b2"], g, nb, lam, 1.0)
+    exact = ob.filter_backward(*args)
+    assert "allow_dx" not in exact
+    ref = ob.filter_backward(*args, band=0.05)
+    alt = ob.filter_backward(*args, decide="bf16")
+    moved = 0
+    for k in ("dx", "dw1", "db1", "dw2", "db2"):
+        assert np.array_equal(ref[k], exact[k])
+        d = np.abs(alt[k] - ref[k])
+        moved += int(np.count_nonzero(d > 1e-12))
+        assert np.all(d <= ref["allow_" + k] + 1e-12), k
+    assert moved > 0 and ref["n_kinks"] > 0   # some decisions did flip
