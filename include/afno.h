@@ -105,6 +105,39 @@ int afno_filter_stage(const void* x, const void* w1, const void* b1, const void*
                       int stage, float* dst, hipStream_t stream);
 
 /*
+ * afno_filter_backward -- gradients of a loss L through out = x + filter(x), given
+ * gout = dL/dout: the transpose of the filter's forward map (the paper trains through it:
+ * "Implementation Details" (a), (e)), step by step in reverse order.  With X the forward
+ * spectrum, v = X w1 + b1, h = relu(v), o = h w2 + b2 per kept mode and block as above:
+ *   dz  = c_kw F(gout)            (F the forward 2-D transform, c_kw its inverse's weights)
+ *   do  = dz where |o| > lambda on that component and the mode is kept, else 0
+ *   dh  = do w2^H (conjugate transpose),  dv = dh where v > 0 on that component, else 0
+ *   dx  = gout + F^T(dv w1^H)     (F^T: the inverse with unit weights c_kw = 1)
+ *   dw1 = sum over kept modes of conj(X)^T dv,  db1 = sum of dv
+ *   dw2 = sum over kept modes of conj(h)^T do,  db2 = sum of do
+ * (re, im pairs hold d/d re and d/d im; relu'(0) = 0 and the softshrink slope is 0 on
+ * [-lambda, lambda]).
+ *   x, w1, b1, w2, b2, sizes, lambda, keep_fraction, dtype   as afno_filter_forward
+ *   gout [B][H][W][C]        dtype, device memory
+ *   dx   [B][H][W][C]        dtype, device memory
+ *   dw1, dw2 [nb][bs][bs][2]  float32, device memory, overwritten (not accumulated)
+ *   db1, db2 [nb][bs][2]      float32, device memory, overwritten
+ * No output may overlap an input or another output (AFNO_ERR_ALIAS).  The library
+ * allocates stream-ordered workspace on `stream`: two spectra, the conjugate-transposed
+ * weights, four per-mode factor tensors of nb * 2 bs * B * kept_w * ceil32(ceil16(H)) values
+ * in dtype, and 2 nb (2 bs)^2 float32 sums.  B == 0 or nothing kept: dx = gout and zero weight
+ * and bias gradients.  Errors as afno_filter_forward; AFNO_ERR_UNSUPPORTED also when a
+ * column of the backward kernel (one tile of H x bs complex values plus two bit masks)
+ * does not fit the LDS.  Weight gradients are sums of fp32 atomic additions: their last
+ * bits may differ between calls.
+ */
+int afno_filter_backward(const void* x, const void* w1, const void* b1, const void* w2,
+                         const void* b2, const void* gout, int64_t B, int64_t H, int64_t W,
+                         int64_t C, int64_t num_blocks, float lambda, float keep_fraction,
+                         int dtype, void* dx, float* dw1, float* db1, float* dw2, float* db2,
+                         hipStream_t stream);
+
+/*
  * Diagnostic per-kernel timing.  afno_profile_begin(max_calls) creates HIP events for
  * up to max_calls filter calls (process-wide); each later afno_filter_forward call
  * records an event before its first kernel and after each of its four phases, on the

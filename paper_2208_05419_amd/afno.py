@@ -27,8 +27,8 @@ AFNO_PATH_AUTO = 0
 AFNO_PATH_GENERIC = 1
 AFNO_PATH_VALU_DFT = 2
 
-EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_profile_begin", "afno_profile_end",
-            "afno_set_kernel_path", "afno_last_error", "afno_version")
+EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_filter_backward", "afno_profile_begin",
+            "afno_profile_end", "afno_set_kernel_path", "afno_last_error", "afno_version")
 KERNELS = ("prep", "row_r2c", "column", "row_c2r")
 
 _ERR_NAMES = {AFNO_ERR_INVALID_ARG: "AFNO_ERR_INVALID_ARG", AFNO_ERR_UNSUPPORTED: "AFNO_ERR_UNSUPPORTED",
@@ -66,6 +66,10 @@ def load_library():
     lib.afno_filter_stage.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
                                       ctypes.c_int, ctypes.c_int, vp, vp]
     lib.afno_filter_stage.restype = ctypes.c_int
+    # the float* gradient outputs are device addresses: passed as plain pointers
+    lib.afno_filter_backward.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
+                                         ctypes.c_int, vp, vp, vp, vp, vp, vp]
+    lib.afno_filter_backward.restype = ctypes.c_int
     lib.afno_last_error.argtypes = []
     lib.afno_last_error.restype = ctypes.c_char_p
     lib.afno_version.argtypes = []
@@ -104,6 +108,13 @@ def afno_filter_stage(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fract
                       stage, dst, stream) -> int:
     return load_library().afno_filter_stage(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam,
                                             keep_fraction, dtype, stage, dst, stream)
+
+
+def afno_filter_backward(x, w1, b1, w2, b2, gout, B, H, W, C, num_blocks, lam, keep_fraction,
+                         dtype, dx, dw1, db1, dw2, db2, stream) -> int:
+    return load_library().afno_filter_backward(x, w1, b1, w2, b2, gout, B, H, W, C, num_blocks,
+                                               lam, keep_fraction, dtype, dx, dw1, db1, dw2,
+                                               db2, stream)
 
 
 def afno_profile_begin(max_calls: int) -> int:
@@ -179,6 +190,25 @@ def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction
                              _stream(stream))
     _check(rc)
     return out
+
+
+def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep_fraction: float = 1.0,
+                    stream=None):
+    """Gradients through out = x + AFNO filter(x) for dL/dout = gout: returns a dict with dx
+    (x's dtype) and dw1, db1, dw2, db2 (float32, the weights' layouts)."""
+    import torch
+    B, H, W, C = x.shape
+    f32 = dict(dtype=torch.float32, device=x.device)
+    dx = torch.empty_like(x)
+    dw1, dw2 = torch.empty(w1.shape, **f32), torch.empty(w2.shape, **f32)
+    db1, db2 = torch.empty(b1.shape, **f32), torch.empty(b2.shape, **f32)
+    if gout.shape != x.shape or gout.dtype != x.dtype:
+        raise ValueError("gout must have x's shape and dtype")
+    rc = afno_filter_backward(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(gout), B, H,
+                              W, C, num_blocks, lam, keep_fraction, _dtype_code(x), _ptr(dx),
+                              _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _stream(stream))
+    _check(rc)
+    return {"dx": dx, "dw1": dw1, "db1": db1, "dw2": dw2, "db2": db2}
 
 
 def filter_stage(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction: float, stage: int,

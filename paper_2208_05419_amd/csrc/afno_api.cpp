@@ -213,6 +213,72 @@ int run(const Args& a, int stage, float* dst, hipStream_t stream) {
   return AFNO_OK;
 }
 
+// the backward pass: validation beyond the forward's, workspace layout, launches
+int run_backward(const Args& a, const void* gout, float* dw1, float* db1, float* dw2, float* db2,
+                 hipStream_t stream) {
+  afno::Plan pl;
+  int rc = make_plan(a, pl);
+  if (rc != AFNO_OK) return rc;
+  if (a.B > 0 && !gout) return fail(AFNO_ERR_INVALID_ARG, "null pointer argument");
+  if (!dw1 || !db1 || !dw2 || !db2) return fail(AFNO_ERR_INVALID_ARG, "null pointer argument");
+  const size_t es = a.dtype == AFNO_DTYPE_FP32 ? 4 : 2;
+  const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;
+  if (a.B > 0 && !aligned(gout, 16)) return fail(AFNO_ERR_UNSUPPORTED, "gout must be 16-byte aligned");
+  if (!aligned(dw1, 4) || !aligned(db1, 4) || !aligned(dw2, 4) || !aligned(db2, 4))
+    return fail(AFNO_ERR_UNSUPPORTED, "weight and bias gradients must be 4-byte aligned");
+  const size_t wgb = (size_t)a.nb * pl.bs * pl.bs * 2 * 4, bgb = (size_t)a.nb * pl.bs * 2 * 4;
+  const size_t wb = (size_t)a.nb * pl.bs * pl.bs * 2 * es, bb = (size_t)a.nb * pl.bs * 2 * es;
+  struct R { const void* p; size_t n; };
+  const R ins[] = {{a.x, xb}, {gout, xb}, {a.w1, wb}, {a.b1, bb}, {a.w2, wb}, {a.b2, bb}};
+  const R outs[] = {{a.out, xb}, {dw1, wgb}, {db1, bgb}, {dw2, wgb}, {db2, bgb}};
+  for (const R& o : outs) {
+    if (!o.p || o.n == 0) continue;
+    for (const R& i : ins)
+      if (i.p && i.n && overlaps(o.p, o.n, i.p, i.n))
+        return fail(AFNO_ERR_ALIAS, "an output overlaps an input");
+    for (const R& q : outs)
+      if (&q != &o && q.p && q.n && overlaps(o.p, o.n, q.p, q.n))
+        return fail(AFNO_ERR_ALIAS, "two outputs overlap");
+  }
+  if (a.B > 0 && afno::bwd_lds(pl) > (size_t)afno::kLdsBytes)
+    return fail(AFNO_ERR_UNSUPPORTED, "backward column tile (H x block size) does not fit in LDS");
+
+  std::call_once(g_attr_once, [] {
+    (void)afno::set_kernel_attributes();
+    (void)hipGetLastError();
+  });
+  afno::BwdPtrs bp{a.x, a.w1, a.b1, a.w2, a.b2, gout, a.out, dw1, db1, dw2, db2, nullptr};
+  hipError_t e;
+  if (a.B == 0 || pl.KW == 0) {  // no mode passes the filter: dx = g, zero gradients
+    e = afno::launch_zero_grads(pl, bp, stream);
+    if (e == hipSuccess && a.B > 0) e = hipMemcpyAsync(a.out, gout, xb, hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
+    return AFNO_OK;
+  }
+  // workspace: Sx, Sg, conjugate-transposed weights, per-mode factors, fp32 product sums
+  auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+  pl.bwd.sx_offset = 0;
+  pl.bwd.sg_offset = up(pl.spec_bytes);
+  pl.bwd.wt_offset = pl.bwd.sg_offset + up(pl.spec_bytes);
+  pl.bwd.modes_offset = pl.bwd.wt_offset + up(2 * wb);
+  const size_t modes_bytes = (size_t)4 * a.nb * 2 * pl.bs * (size_t)afno::bwd_mpad(pl) * es;
+  pl.bwd.acc_offset = pl.bwd.modes_offset + up(modes_bytes);
+  pl.bwd.bytes = pl.bwd.acc_offset + (size_t)2 * a.nb * (2 * pl.bs) * (2 * pl.bs) * 4;
+  void* ws = nullptr;
+  e = hipMallocAsync(&ws, pl.bwd.bytes, stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") + std::to_string(pl.bwd.bytes) +
+                                  " bytes: " + hipGetErrorString(e));
+  }
+  bp.ws = ws;
+  e = afno::launch_backward(pl, bp, stream);
+  hipError_t ef = hipFreeAsync(ws, stream);
+  if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
+  if (ef != hipSuccess) return fail(AFNO_ERR_HIP, std::string("workspace free: ") + hipGetErrorString(ef));
+  return AFNO_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -241,6 +307,16 @@ int afno_filter_stage(const void* x, const void* w1, const void* b1, const void*
   Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, dst,
          B > 0 && H > 0 && W > 0 && C > 0 ? nd * sizeof(float) : 0};
   return run(a, stage, dst, stream);
+}
+
+int afno_filter_backward(const void* x, const void* w1, const void* b1, const void* w2,
+                         const void* b2, const void* gout, int64_t B, int64_t H, int64_t W,
+                         int64_t C, int64_t num_blocks, float lambda, float keep_fraction,
+                         int dtype, void* dx, float* dw1, float* db1, float* dw2, float* db2,
+                         hipStream_t stream) {
+  g_last_error.clear();
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, dx, 0};
+  return run_backward(a, gout, dw1, db1, dw2, db2, stream);
 }
 
 int afno_profile_begin(int max_calls) {

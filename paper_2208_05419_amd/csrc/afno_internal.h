@@ -54,6 +54,17 @@ struct Plan {
   size_t frag_offset; // fragment-ordered weights (size-specialised column kernels), after S
   size_t tab_offset;  // transform table (MFMA-transform column kernel), after the weights
   size_t ws_bytes;    // whole workspace
+  struct {            // backward-pass workspace offsets (afno_filter_backward)
+    size_t sx_offset, sg_offset, wt_offset, modes_offset, acc_offset, bytes;
+  } bwd;
+};
+
+// pointers of one backward call (dw*, db* float32)
+struct BwdPtrs {
+  const void *x, *w1, *b1, *w2, *b2, *gout;
+  void* dx;
+  float *dw1, *db1, *dw2, *db2;
+  void* ws;
 };
 
 hipError_t set_kernel_attributes();
@@ -68,6 +79,11 @@ bool use_fast_col(const Plan& pl);  // under the current kernel path
 size_t frag_bytes(const Plan& pl);
 size_t mfma_tab_bytes(const Plan& pl);
 // ev: NULL, or kProfEvents events recorded before the first kernel and after each phase
+// backward pass: modes per block of the per-mode factor tensors, and the column kernel's LDS
+int64_t bwd_mpad(const Plan& pl);
+size_t bwd_lds(const Plan& pl);
+hipError_t launch_backward(const Plan& pl, const BwdPtrs& a, hipStream_t st);
+hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,
                          int stage, hipStream_t st, hipEvent_t* ev);

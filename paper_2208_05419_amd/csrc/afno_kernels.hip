@@ -25,6 +25,7 @@
 #include "kernels_fast.h"
 #include "kernels_generic.h"
 #include "kernels_mfma.h"
+#include "kernels_backward.h"
 
 namespace afno {
 
@@ -243,6 +244,93 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   return e;
 }
 
+// ------------------------------------------------------------------ backward pass
+
+int64_t bwd_mpad(const Plan& pl) { return pl.B * pl.KW * (int64_t)col_bwd_hc((int)pl.col.H16); }
+size_t bwd_lds(const Plan& pl) { return col_bwd_lds(pl.col); }
+
+// The W-axis forward transform of x into S (no operand preparation).
+template <typename T>
+static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream_t st) {
+  if (g_kernel_path != 1 && fast_row_available(pl.W, pl.C)) {
+    PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0};
+    launch_row_fwd_fast<T>(pl, x, S, pj, st);
+  } else {
+    dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
+    hipLaunchKernelGGL(row_r2c_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, x, S, pl.row);
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
+  const T* x = static_cast<const T*>(a.x);
+  const T* g = static_cast<const T*>(a.gout);
+  char* ws = static_cast<char*>(a.ws);
+  T* Sx = reinterpret_cast<T*>(ws + pl.bwd.sx_offset);
+  T* Sg = reinterpret_cast<T*>(ws + pl.bwd.sg_offset);
+  T* wt1 = reinterpret_cast<T*>(ws + pl.bwd.wt_offset);
+  T* wt2 = wt1 + pl.nb * pl.bs * pl.bs * 2;
+  T* modes = reinterpret_cast<T*>(ws + pl.bwd.modes_offset);
+  float* acc = reinterpret_cast<float*>(ws + pl.bwd.acc_offset);
+  const int nb = (int)pl.nb, bs = (int)pl.bs;
+  const int64_t mpad = bwd_mpad(pl);
+  hipError_t e = launch_row_forward<T>(pl, x, Sx, st);
+  if (e == hipSuccess) e = launch_row_forward<T>(pl, g, Sg, st);
+  if (e != hipSuccess) return e;
+  const int64_t nw = (int64_t)2 * nb * bs * bs;
+  hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
+                     dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
+                     wt1, wt2, nb, bs);
+  const int64_t nacc = (int64_t)2 * nb * (2 * bs) * (2 * bs);
+  hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nacc + 255) / 256, 4096)),
+                     dim3(256), 0, st, acc, nacc);
+  hipLaunchKernelGGL(column_bwd_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
+                     dim3(pl.col_threads), bwd_lds(pl), st, Sx, Sg, static_cast<const T*>(a.w1),
+                     static_cast<const T*>(a.b1), static_cast<const T*>(a.w2),
+                     static_cast<const T*>(a.b2), wt1, wt2, pl.col, modes, mpad, (int)pl.W);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // weight gradients: K split in chunks of whole 32-mode steps, a few per output tile
+  const int nt64 = (2 * bs + 63) / 64;
+  const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
+  const int kchunk = (int)(((mpad + nk - 1) / nk + 31) / 32 * 32);
+  const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)((mpad + kchunk - 1) / kchunk));
+  hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kchunk, acc);
+  hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
+                     0, st, acc, nb, bs, a.dw1, a.dw2);
+  hipLaunchKernelGGL(bias_grad_kernel<T>, dim3((unsigned)(2 * nb * 2 * bs)), dim3(256), 0, st, modes,
+                     mpad, nb, bs, a.db1, a.db2);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // dx = g + C2R(Sg): the W-axis inverse with g as the residual
+  T* dx = static_cast<T*>(a.dx);
+  if (g_kernel_path != 1 && fast_row_available(pl.W, pl.C))
+    launch_row_inv_fast<T>(pl, Sg, g, dx, nullptr, 0, st);
+  else {
+    dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
+    hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, Sg, g, dx,
+                       nullptr, pl.row, 0);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_backward(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
+  if (pl.dtype == 0) return launch_bwd<float>(pl, a, st);
+  return launch_bwd<bf16>(pl, a, st);
+}
+
+// zero weight and bias gradients (a call whose modes are all cut off)
+hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
+  const int64_t nw = pl.nb * pl.bs * pl.bs * 2, nbias = pl.nb * pl.bs * 2;
+  const unsigned g = (unsigned)std::min<int64_t>((nw + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_zero_f32<float>, dim3(g), dim3(256), 0, st, a.dw1, nw);
+  hipLaunchKernelGGL(fill_zero_f32<float>, dim3(g), dim3(256), 0, st, a.dw2, nw);
+  hipLaunchKernelGGL(fill_zero_f32<float>, dim3(1), dim3(256), 0, st, a.db1, nbias);
+  hipLaunchKernelGGL(fill_zero_f32<float>, dim3(1), dim3(256), 0, st, a.db2, nbias);
+  return hipGetLastError();
+}
+
 hipError_t set_kernel_attributes() {
   const int lds_max = kLdsBytes;
   hipError_t e, first = hipSuccess;
@@ -256,6 +344,8 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(row_c2r_kernel<bf16>)
   AFNO_ATTR(column_kernel<float>)
   AFNO_ATTR(column_kernel<bf16>)
+  AFNO_ATTR(column_bwd_kernel<float>)
+  AFNO_ATTR(column_bwd_kernel<bf16>)
   AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))

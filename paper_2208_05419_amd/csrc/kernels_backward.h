@@ -1,0 +1,421 @@
+// kernels_backward.h -- the AFNO filter's backward pass on gfx950.
+//
+// For an upstream gradient g = dL/dout the filter's transpose runs the forward steps in
+// reverse ("Model Innovations", steps 1-3; the paper trains through them, "Implementation
+// Details" (a), (e)).  With F the 2-D real DFT (W-axis R2C then H-axis DFT, ortho), G its
+// half-spectrum inverse (H-axis inverse DFT then W-axis C2R with weights c_kw = 1 at kw = 0
+// and W/2, else 2) and the per-mode block MLP v = X W1 + b1, h = relu(v), o = h W2 + b2,
+// z = S_lam(o) (componentwise on re and im, zero outside the cutoff), y = G(z):
+//
+//   dz  = c_kw F(g)                       (G's transpose: the weighted C2R's is c_kw R2C,
+//                                          the unitary inverse H-DFT's the forward H-DFT)
+//   do  = dz where |o| > lam and the mode is kept, else 0   (componentwise)
+//   dh  = do W2^H,   dv = dh where v > 0, else 0
+//   dX  = dv W1^H
+//   dx  = g + G(dX / c_kw)                (F's transpose: C2R with unit weights)
+//   dW1 = sum over modes conj(X)^T dv,  db1 = sum dv;  dW2 = sum conj(h)^T do,  db2 = sum do
+//
+// Passes: the forward W-axis kernel on x and on g (spectra Sx, Sg); column_bwd_kernel per
+// (b, kw, block) recomputes X, h and both masks, transforms the gradient column and runs
+// the two conjugate-transposed products, writing dX's inverse back into Sg and the per-mode
+// factors X, h, do, dv to HBM mode-contiguous; wgrad_kernel reduces the weight gradients
+// over all modes on the matrix cores; row sums give the bias gradients; the forward W-axis
+// inverse kernel with g as its residual gives dx.
+#pragma once
+#include "kernels_generic.h"
+
+namespace afno {
+
+// wt[k][j][i] = conj(w[k][i][j]) for both layers: x wt = x W^H on the block_gemm path
+template <typename T>
+__global__ void __launch_bounds__(256) conj_transpose_weights(const T* __restrict__ w1,
+                                                              const T* __restrict__ w2,
+                                                              T* __restrict__ wt1,
+                                                              T* __restrict__ wt2, int nb, int bs) {
+  const int64_t n = (int64_t)nb * bs * bs;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int layer = t >= n ? 1 : 0;
+    const int64_t u = t - layer * n;
+    const int64_t k = u / ((int64_t)bs * bs);
+    const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
+    const T* src = (layer ? w2 : w1) + ((k * bs + i) * bs + j) * 2;
+    T* dst = (layer ? wt2 : wt1) + ((k * bs + j) * bs + i) * 2;
+    dst[0] = src[0];
+    dst[1] = Store<T>::to(-ld_f(src + 1));
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) fill_zero_f32(float* __restrict__ p, int64_t n) {
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n;
+       t += (int64_t)gridDim.x * blockDim.x)
+    p[t] = 0.f;
+}
+
+// Per-mode factors: four tensors [4][nb][2 bs][mpad] in T (X, h, do, dv), entry-major with the
+// modes contiguous; the column (b, kw) holds modes (b KW + kw) HC .. + HC - 1, HC = H16
+// rounded up to 32 (rows past H hold X = 0, do = dv = 0, so they add nothing to the sums);
+// mpad = B KW HC, a multiple of the bf16 product's 32-mode k-step.
+enum { kModeX = 0, kModeH = 1, kModeDo = 2, kModeDv = 3 };
+
+// tile rows 0 .. HC - 1 of the block's 2 bs entries -> dst[e][m0 + row], 8 rows per task
+// (rows past H16 are zero)
+template <typename T>
+__device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int HC, int bs,
+                                            T* dst, int64_t mpad, int64_t m0) {
+  const int tasks = bs * (HC / 8);
+  for (int t = threadIdx.x; t < tasks; t += blockDim.x) {
+    const int c = t % bs, r0 = 8 * (t / bs);
+    float re[8], im[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float2 z = r0 < H16 ? ld_c(tile + (r0 + i) * ldt + 2 * c) : make_float2(0.f, 0.f);
+      re[i] = z.x;
+      im[i] = z.y;
+    }
+    T* pr = dst + (int64_t)(2 * c) * mpad + m0 + r0;
+    T* pi = pr + mpad;
+    if constexpr (sizeof(T) == 2) {
+      union { uint4 u; bf16 h[8]; } a, b;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        a.h[i] = (bf16)re[i];
+        b.h[i] = (bf16)im[i];
+      }
+      *reinterpret_cast<uint4*>(pr) = a.u;
+      *reinterpret_cast<uint4*>(pi) = b.u;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; i += 4) {
+        *reinterpret_cast<float4*>(pr + i) = make_float4(re[i], re[i + 1], re[i + 2], re[i + 3]);
+        *reinterpret_cast<float4*>(pi + i) = make_float4(im[i], im[i + 1], im[i + 2], im[i + 3]);
+      }
+    }
+  }
+}
+
+// one column's rows h < H from S into the tile (times scale), padding rows zero
+template <typename T>
+__device__ __forceinline__ void load_column(T* tile, const T* col, int64_t row_stride, int ldt,
+                                            int H, int H16, int bs, float scale) {
+  for (int it = threadIdx.x; it < H16 * bs; it += blockDim.x) {
+    const int h = it / bs, c = it - h * bs;
+    float2 z = make_float2(0.f, 0.f);
+    if (h < H) {
+      z = ld_c(col + h * row_stride + 2 * c);
+      z.x *= scale;
+      z.y *= scale;
+    }
+    st_c(tile + h * ldt + 2 * c, z);
+  }
+}
+
+// DFT along H of the tile's rows h < H (forward or inverse), chk channels at a time through
+// the float buffer, scaled by 1/sqrt(H)
+template <typename T, bool INV>
+__device__ __forceinline__ void dft_tile(T* tile, float2* fbuf, const float2* tw, const ColParams& p) {
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int chk = p.chk, H = p.H, ldt = p.ldt;
+  const int sig = tid % chk, sub = tid / chk, nsub = nthr / chk;
+  for (int cc = 0; cc < p.bs; cc += chk) {
+    for (int it = tid; it < H * chk; it += nthr) {
+      const int h = it / chk, q = it - h * chk;
+      fbuf[h * chk + q] = ld_c(tile + h * ldt + 2 * (cc + q));
+    }
+    __syncthreads();
+    fft_lds<kColEmax, INV>(fbuf, chk, p.rh, sig, sub, nsub, tw);
+    for (int it = tid; it < H * chk; it += nthr) {
+      const int h = it / chk, q = it - h * chk;
+      const float2 z = fbuf[h * chk + q];
+      st_c(tile + h * ldt + 2 * (cc + q), make_float2(z.x * p.inv_sqrt_h, z.y * p.inv_sqrt_h));
+    }
+    __syncthreads();
+  }
+}
+
+// LDS of column_bwd_kernel: the tile, two bit masks [H16][2 bs / 32] words (word w of a row
+// holds real columns 32 w .. 32 w + 31, the columns one MFMA wave owns), the float buffer,
+// the twiddles
+__host__ __device__ inline size_t col_bwd_mask_bytes(const ColParams& p) {
+  return ((size_t)p.H16 * (2 * p.bs / 32) * 4 + 15) / 16 * 16;
+}
+__host__ __device__ inline size_t col_bwd_lds(const ColParams& p) {
+  return (size_t)p.tile_bytes + 2 * col_bwd_mask_bytes(p) + (size_t)p.H * p.chk * 8 + (size_t)p.H * 8;
+}
+__host__ __device__ inline int col_bwd_hc(int H16) { return (H16 + 31) / 32 * 32; }
+
+// the 32 mask bits of a row for the wave's two 16-column tiles: bit l16 from column tile 0,
+// bit l16 + 16 from tile 1; lane l16 == 0 of each 16-lane group holds its row's word
+__device__ __forceinline__ uint32_t mask_word(bool p0, bool p1, int lane) {
+  const unsigned long long b0 = __ballot(p0), b1 = __ballot(p1);
+  const int g = lane >> 4;
+  return (uint32_t)((b0 >> (16 * g)) & 0xffffull) | ((uint32_t)((b1 >> (16 * g)) & 0xffffull) << 16);
+}
+
+// grid B * KW * nb (block index fastest), block 64 * max(bs / 16, 4), dynamic LDS
+// col_bwd_lds(p).  Sx: the forward spectrum of x; Sg: that of g, replaced by
+// G^-1-side gradient dX' = IDFT_H(dX) / c_kw (so that the forward C2R kernel's c_kw weights
+// give the unit-weight transpose); modes: the four per-mode factor tensors.
+template <typename T>
+__global__ void __launch_bounds__(kColMaxThreads)
+column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restrict__ w1,
+                  const T* __restrict__ b1, const T* __restrict__ w2, const T* __restrict__ b2,
+                  const T* __restrict__ wt1, const T* __restrict__ wt2, ColParams p,
+                  T* __restrict__ modes, int64_t mpad, int W) {
+  extern __shared__ float4 smem_raw[];
+  T* tile = reinterpret_cast<T*>(smem_raw);
+  const size_t mk_bytes = col_bwd_mask_bytes(p);
+  uint32_t* mk1 = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(smem_raw) + p.tile_bytes);  // v > 0
+  uint32_t* mk2 = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(mk1) + mk_bytes);  // |o| > lam, kept
+  float2* fbuf = reinterpret_cast<float2*>(reinterpret_cast<char*>(mk2) + mk_bytes);
+  float2* tw = fbuf + (size_t)p.H * p.chk;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15;
+  const int bs = p.bs, ldt = p.ldt, H = p.H, H16 = p.H16, nb2 = 2 * bs, nw = nb2 / 32;
+  const int HC = col_bwd_hc(H16);
+
+  const int blk = blockIdx.x % p.nb;
+  const int rest = blockIdx.x / p.nb;
+  const int kw = rest % p.KW;
+  const int64_t b = rest / p.KW;
+  const int64_t row_stride = (int64_t)p.KW * p.C * 2;
+  const int64_t coff = ((b * H) * p.KW + kw) * (int64_t)p.C * 2 + (int64_t)blk * bs * 2;
+  const int64_t m0 = (b * p.KW + kw) * (int64_t)HC;
+  auto mode_tensor = [&](int t) { return modes + ((int64_t)t * p.nb + blk) * nb2 * mpad; };
+  const float ckw = (kw == 0 || 2 * kw == W) ? 1.f : 2.f;
+
+  make_twiddles(tw, H);
+
+  const int mt = H16 / 16;
+  uint32_t live = 0;
+  for (int m = 0; m < mt; ++m) {
+    bool any = false;
+    for (int r = 16 * m; r < 16 * m + 16; ++r) any |= row_kept(r, H, p.kept_h);
+    live |= (any ? 1u : 0u) << m;
+  }
+  const bool active = wave < bs / 16;
+  const int nu0 = 32 * wave + (lane & 15);  // real output column of tile 0 (tile 1: +16)
+  f32x4 acc[kColMaxMTiles][2];
+
+  // ---- X = F(x) column; write X
+  load_column<T>(tile, Sx + coff, row_stride, ldt, H, H16, bs, 1.f);
+  __syncthreads();
+  dft_tile<T, false>(tile, fbuf, tw, p);
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeX), mpad, m0);
+
+  // ---- layer 1: h = relu(X W1 + b1) -> tile, mask v > 0
+  if (active) block_gemm<T>(tile, ldt, w1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
+  __syncthreads();  // the tile's X rows are read (products and the X write)
+  if (active) {
+    const T* B1 = b1 + (int64_t)blk * bs * 2;
+    const float bia0 = ld_f(B1 + nu0), bia1 = ld_f(B1 + nu0 + 16);
+#pragma unroll
+    for (int m = 0; m < kColMaxMTiles; ++m) {
+      if (m >= mt) continue;
+      const bool lv = (live >> m) & 1u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        const float v0 = acc[m][0][r] + bia0, v1 = acc[m][1][r] + bia1;
+        if (lv) {
+          tile[row * ldt + nu0] = Store<T>::to(fmaxf(v0, 0.f));
+          tile[row * ldt + nu0 + 16] = Store<T>::to(fmaxf(v1, 0.f));
+        }
+        const uint32_t wd = mask_word(lv && v0 > 0.f, lv && v1 > 0.f, lane);
+        if (l16 == 0) mk1[row * nw + wave] = wd;
+      }
+    }
+  }
+  __syncthreads();
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeH), mpad, m0);
+
+  // ---- layer 2: only its mask |o| > lam (and the cutoff) is needed
+  if (active) block_gemm<T>(tile, ldt, w2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
+  if (active) {
+    const T* B2 = b2 + (int64_t)blk * bs * 2;
+    const float bia0 = ld_f(B2 + nu0), bia1 = ld_f(B2 + nu0 + 16);
+#pragma unroll
+    for (int m = 0; m < kColMaxMTiles; ++m) {
+      if (m >= mt) continue;
+      const bool lv = (live >> m) & 1u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        const bool keep = lv && row_kept(row, H, p.kept_h);
+        const uint32_t wd = mask_word(keep && fabsf(acc[m][0][r] + bia0) > p.lam,
+                                      keep && fabsf(acc[m][1][r] + bia1) > p.lam, lane);
+        if (l16 == 0) mk2[row * nw + wave] = wd;
+      }
+    }
+  }
+  __syncthreads();  // the h rows are read (products and the h write), masks complete
+
+  // ---- dz = c_kw F(g) column; do = dz masked; write do
+  load_column<T>(tile, Sg + coff, row_stride, ldt, H, H16, bs, ckw);
+  __syncthreads();
+  dft_tile<T, false>(tile, fbuf, tw, p);
+  for (int it = tid; it < H16 * nb2; it += blockDim.x) {
+    const int row = it / nb2, e = it - row * nb2;
+    if (!((mk2[row * nw + (e >> 5)] >> (e & 31)) & 1u)) tile[row * ldt + e] = Store<T>::to(0.f);
+  }
+  __syncthreads();
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDo), mpad, m0);
+
+  // ---- dv = (do W2^H) masked by v > 0; write dv
+  if (active) block_gemm<T>(tile, ldt, wt2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
+  __syncthreads();
+  if (active) {
+#pragma unroll
+    for (int m = 0; m < kColMaxMTiles; ++m) {
+      if (m >= mt) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        const uint32_t wd = mk1[row * nw + wave];  // 0 on rows outside the live tiles
+        tile[row * ldt + nu0] = Store<T>::to((wd >> l16) & 1u ? acc[m][0][r] : 0.f);
+        tile[row * ldt + nu0 + 16] = Store<T>::to((wd >> (l16 + 16)) & 1u ? acc[m][1][r] : 0.f);
+      }
+    }
+  }
+  __syncthreads();
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDv), mpad, m0);
+
+  // ---- dX = dv W1^H -> inverse H-DFT -> Sg column / c_kw
+  if (active) block_gemm<T>(tile, ldt, wt1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
+  __syncthreads();
+  if (active) {
+#pragma unroll
+    for (int m = 0; m < kColMaxMTiles; ++m) {
+      if (m >= mt) continue;
+      const bool lv = (live >> m) & 1u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * m + 4 * (lane >> 4) + r;
+        tile[row * ldt + nu0] = Store<T>::to(lv ? acc[m][0][r] : 0.f);
+        tile[row * ldt + nu0 + 16] = Store<T>::to(lv ? acc[m][1][r] : 0.f);
+      }
+    }
+  }
+  __syncthreads();
+  dft_tile<T, true>(tile, fbuf, tw, p);
+  T* col = Sg + coff;
+  const float inv_c = 1.f / ckw;
+  for (int it = tid; it < H * bs; it += blockDim.x) {
+    const int h = it / bs, c = it - h * bs;
+    const float2 z = ld_c(tile + h * ldt + 2 * c);
+    st_c(col + h * row_stride + 2 * c, make_float2(z.x * inv_c, z.y * inv_c));
+  }
+}
+
+// Weight-gradient products over all modes: for layer 0 (dW1) A = X, B = dv; for layer 1
+// (dW2) A = h, B = do; acc[layer][blk][r][s] += sum over the workgroup's mode range of
+// A[r][m] B[s][m] (r, s the 2 bs real entries, (c, rho) interleaved), fp32 atomics.
+// grid (2 nb tiles64^2, ceil(mpad / kchunk)), 256 threads: four waves with 32 x 32 each of
+// a 64 x 64 output tile; kchunk a multiple of 32.
+template <typename T>
+__global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes, int64_t mpad,
+                                                    int nb, int bs, int kchunk,
+                                                    float* __restrict__ acc_out) {
+  typedef Mma<T> M;
+  const int nb2 = 2 * bs;
+  const int nt64 = (nb2 + 63) / 64;
+  int g = blockIdx.x;
+  const int ts = g % nt64; g /= nt64;
+  const int tr = g % nt64; g /= nt64;
+  const int blk = g % nb; g /= nb;
+  const int layer = g;  // 0: dW1, 1: dW2
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = 64 * tr + 32 * (wave >> 1), s0 = 64 * ts + 32 * (wave & 1);
+  const T* A = modes + ((int64_t)(layer ? kModeH : kModeX) * nb + blk) * nb2 * mpad;
+  const T* Bm = modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * nb2 * mpad;
+  const int64_t k0 = (int64_t)blockIdx.y * kchunk;
+  const int64_t k1 = k0 + kchunk < mpad ? k0 + kchunk : mpad;
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bool rv[2] = {r0 < nb2, r0 + 16 < nb2}, sv[2] = {s0 < nb2, s0 + 16 < nb2};
+  const int l16 = lane & 15, gq = lane >> 4;
+  for (int64_t k = k0; k < k1; k += M::kK) {
+    typename M::Frag a[2], bfr[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = rv[i] ? r0 + 16 * i + l16 : 0;
+      const int s = sv[i] ? s0 + 16 * i + l16 : 0;
+      if constexpr (sizeof(T) == 2) {
+        a[i] = *reinterpret_cast<const bf16x8*>(A + (int64_t)r * mpad + k + 8 * gq);
+        bfr[i] = *reinterpret_cast<const bf16x8*>(Bm + (int64_t)s * mpad + k + 8 * gq);
+      } else {
+        a[i] = A[(int64_t)r * mpad + k + gq];
+        bfr[i] = Bm[(int64_t)s * mpad + k + gq];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = M::mma(a[i], bfr[j], acc[i][j]);
+  }
+  float* out = acc_out + ((int64_t)layer * nb + blk) * nb2 * nb2;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (!rv[i] || !sv[j]) continue;
+      const int s = s0 + 16 * j + l16;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = r0 + 16 * i + 4 * gq + q;
+        unsafeAtomicAdd(out + (int64_t)r * nb2 + s, acc[i][j][q]);  // device memory
+      }
+    }
+}
+
+// dW (re, im) from the real-entry products: for entries r = (i, rho), s = (j, sigma),
+// dW[i][j] = (P[(i,0)][(j,0)] + P[(i,1)][(j,1)], P[(i,0)][(j,1)] - P[(i,1)][(j,0)])
+// (conj(a) b summed); grid over 2 nb bs^2.
+__global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ acc_in, int nb,
+                                                      int bs, float* __restrict__ dw1,
+                                                      float* __restrict__ dw2) {
+  const int nb2 = 2 * bs;
+  const int64_t n = (int64_t)nb * bs * bs;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int layer = t >= n ? 1 : 0;
+    const int64_t u = t - layer * n;
+    const int64_t k = u / ((int64_t)bs * bs);
+    const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
+    const float* P = acc_in + ((int64_t)layer * nb + k) * nb2 * nb2;
+    const float rr = P[(2 * i) * nb2 + 2 * j], ii = P[(2 * i + 1) * nb2 + 2 * j + 1];
+    const float ri = P[(2 * i) * nb2 + 2 * j + 1], ir = P[(2 * i + 1) * nb2 + 2 * j];
+    float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
+    d[0] = rr + ii;
+    d[1] = ri - ir;
+  }
+}
+
+// bias gradients: db[blk][j][rho] = sum over modes of B[(j, rho)][m]; one workgroup per
+// (layer, blk, entry); layer 0 sums dv (db1), layer 1 sums do (db2)
+template <typename T>
+__global__ void __launch_bounds__(256) bias_grad_kernel(const T* __restrict__ modes, int64_t mpad,
+                                                        int nb, int bs, float* __restrict__ db1,
+                                                        float* __restrict__ db2) {
+  const int nb2 = 2 * bs;
+  const int e = blockIdx.x % nb2;
+  const int blk = (blockIdx.x / nb2) % nb;
+  const int layer = blockIdx.x / (nb2 * nb);
+  const T* row = modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * nb2 * mpad +
+                 (int64_t)e * mpad;
+  float s = 0.f;
+  for (int64_t m = threadIdx.x; m < mpad; m += blockDim.x) s += ld_f(row + m);
+  __shared__ float red[256];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ((layer ? db2 : db1) + (int64_t)blk * nb2)[e] = red[0];
+}
+
+}  // namespace afno

@@ -120,3 +120,33 @@ def test_kernel_path_switch_validation():
     assert afno.afno_set_kernel_path(afno.AFNO_PATH_GENERIC) == afno.AFNO_OK
     assert afno.afno_set_kernel_path(afno.AFNO_PATH_VALU_DFT) == afno.AFNO_OK
     assert afno.afno_set_kernel_path(afno.AFNO_PATH_AUTO) == afno.AFNO_OK
+
+
+G, DX, DW1, DB1, DW2, DB2 = (0x10000000 * (i + 8) for i in range(6))
+
+
+def call_bwd(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, g=G, B=1, H=16, W=32, C=64, nb=4, lam=0.01, keep=1.0,
+             dtype=afno.AFNO_DTYPE_FP32, dx=DX, dw1=DW1, db1=DB1, dw2=DW2, db2=DB2)
+    a.update(kw)
+    return afno.afno_filter_backward(a["x"], a["w1"], a["b1"], a["w2"], a["b2"], a["g"], a["B"],
+                                     a["H"], a["W"], a["C"], a["nb"], a["lam"], a["keep"],
+                                     a["dtype"], a["dx"], a["dw1"], a["db1"], a["dw2"], a["db2"],
+                                     None)
+
+
+@pytest.mark.parametrize("kw", [dict(g=None), dict(dx=None), dict(dw1=None), dict(db2=None),
+                                dict(C=64, nb=3), dict(lam=-1.0)])
+def test_backward_invalid_arguments(kw):
+    assert call_bwd(**kw) == afno.AFNO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(g=G + 8), dict(dw1=DW1 + 2), dict(H=7), dict(C=512, nb=2)])
+def test_backward_unsupported(kw):
+    assert call_bwd(**kw) == afno.AFNO_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kw", [dict(dx=G), dict(dx=X), dict(dw1=W1), dict(dw2=DW1 + 64),
+                                dict(db1=G + 128), dict(db2=DX)])
+def test_backward_alias(kw):
+    assert call_bwd(**kw) == afno.AFNO_ERR_ALIAS
