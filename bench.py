@@ -14,12 +14,13 @@ one event between calls), per-kernel HIP-event times on the launch stream over a
 (the headline timing records no events between its steps),
 the roofline of the dominant kernel (algorithmic bytes or FLOPs per launch divided by
 its mean launch time), measured HBM traffic from stored rocprofv3 counters when they
-belong to the current kernel sources, the 100-member ensemble workload, the other
+belong to the current kernel sources, the backward pass on the same workload (dx and the
+parameter gradients for an upstream gradient), the 100-member ensemble workload, the other
 workloads' throughput, and the float64 CPU oracle timed on a bounded sample on the host
 cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-ensemble] [--no-cpu-baseline]
-                    [--no-others]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-backward] [--no-ensemble]
+                    [--no-cpu-baseline] [--no-others]
 """
 from __future__ import annotations
 
@@ -140,6 +141,54 @@ def time_workload(wl, steps: int, warmup: int, seed: int = 0):
     return total_ms / steps, {k: v / max(calls, 1) for k, v in kernel_ms.items()}, calls, dist
 
 
+def time_backward(wl, steps: int, warmup: int, seed: int = 0):
+    """Mean time of one backward call (dx and the four parameter gradients for an upstream
+    gradient g) with inputs resident in HBM; one event pair around all timed calls."""
+    import numpy as np
+    import torch
+
+    import paper_2208_05419_amd as afno
+    from paper_2208_05419_amd import synth
+
+    def dev(a):
+        if wl.dtype == "fp32":
+            return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    x = dev(synth.make_x(wl, seed=seed))
+    w = {k: dev(v) for k, v in synth.make_weights(wl, seed=seed).items()}
+    g = dev(synth.quantize(np.random.default_rng(1000 + seed).standard_normal(x.shape), wl.dtype))
+    stream = torch.cuda.current_stream()
+
+    def step():
+        afno.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], g, wl.num_blocks, wl.lam,
+                             wl.keep, stream=stream)
+
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < PREWARM_S:
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / steps
+    es = 2 if wl.dtype == "bf16" else 4
+    io_bytes = 3 * wl.B * wl.H * wl.W * wl.C * es   # read x and g, write dx: any backward's floor
+    del x, w, g
+    torch.cuda.empty_cache()
+    return {"workload": wl.name, "samples_per_s": round(wl.B / (ms * 1e-3), 2),
+            "ms_per_step": round(ms, 5), "io_bytes": io_bytes,
+            "io_GB_s": round(io_bytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def roofline(wl, kern_ms: dict, es: int):
     work = algorithmic_work(wl, es)
     if kern_ms.get("prep", 0.0) < 5e-4:
@@ -231,6 +280,9 @@ def main():
     ap.add_argument("--no-ensemble", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true", help="skip the other workloads' timings")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass timing")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time only the backward pass (one JSON object; for kernel traces)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="run one plain copy of this many MiB first (for counter scaling)")
@@ -252,6 +304,9 @@ def main():
         calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[synth.HEADLINE]
     es = 2 if wl.dtype == "bf16" else 4
+    if args.backward_only:
+        print(json.dumps({"backward": time_backward(wl, args.steps, args.warmup)}), flush=True)
+        return
     ms, kern_ms, calls, dist = time_workload(wl, args.steps, args.warmup)
     roof, per_kernel = roofline(wl, kern_ms, es)
     value = wl.B / (ms * 1e-3)
@@ -275,6 +330,8 @@ def main():
         "timed_calls": calls,
         "call_ms": dist,
     }
+    if not args.no_backward:
+        line["backward"] = time_backward(wl, max(args.steps // 2, 10), max(args.warmup // 2, 3))
     if not args.no_ensemble:
         ens = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
         e_ms, e_kern, _, e_dist = time_workload(ens, max(args.steps // 5, 5), max(args.warmup // 5, 3))
