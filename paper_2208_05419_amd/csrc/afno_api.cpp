@@ -255,15 +255,18 @@ int run_backward(const Args& a, const void* gout, float* dw1, float* db1, float*
     if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
     return AFNO_OK;
   }
-  // workspace: Sx, Sg, conjugate-transposed weights, per-mode factors, fp32 product sums
+  // workspace: Sx, Sg, conjugate-transposed weights, the matrix-core kernel's prepared
+  // operands, per-mode factors, fp32 product and bias sums
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
   pl.bwd.sx_offset = 0;
   pl.bwd.sg_offset = up(pl.spec_bytes);
   pl.bwd.wt_offset = pl.bwd.sg_offset + up(pl.spec_bytes);
-  pl.bwd.modes_offset = pl.bwd.wt_offset + up(2 * wb);
+  pl.bwd.prep_offset = pl.bwd.wt_offset + up(2 * wb);
+  pl.bwd.modes_offset = pl.bwd.prep_offset + up(afno::bwd_prep_bytes(pl));
   const size_t modes_bytes = (size_t)4 * a.nb * 2 * pl.bs * (size_t)afno::bwd_mpad(pl) * es;
   pl.bwd.acc_offset = pl.bwd.modes_offset + up(modes_bytes);
-  pl.bwd.bytes = pl.bwd.acc_offset + (size_t)2 * a.nb * (2 * pl.bs) * (2 * pl.bs) * 4;
+  pl.bwd.bytes = pl.bwd.acc_offset + ((size_t)2 * a.nb * (2 * pl.bs) * (2 * pl.bs) +
+                                      (size_t)2 * a.nb * (2 * pl.bs)) * 4;
   void* ws = nullptr;
   e = hipMallocAsync(&ws, pl.bwd.bytes, stream);
   if (e != hipSuccess) {

@@ -55,7 +55,7 @@ struct Plan {
   size_t tab_offset;  // transform table (MFMA-transform column kernel), after the weights
   size_t ws_bytes;    // whole workspace
   struct {            // backward-pass workspace offsets (afno_filter_backward)
-    size_t sx_offset, sg_offset, wt_offset, modes_offset, acc_offset, bytes;
+    size_t sx_offset, sg_offset, wt_offset, prep_offset, modes_offset, acc_offset, bytes;
   } bwd;
 };
 
@@ -82,6 +82,7 @@ size_t mfma_tab_bytes(const Plan& pl);
 // backward pass: modes per block of the per-mode factor tensors, and the column kernel's LDS
 int64_t bwd_mpad(const Plan& pl);
 size_t bwd_lds(const Plan& pl);
+size_t bwd_prep_bytes(const Plan& pl);  // prepared operands of the matrix-core backward
 hipError_t launch_backward(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,

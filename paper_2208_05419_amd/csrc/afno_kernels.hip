@@ -26,6 +26,7 @@
 #include "kernels_generic.h"
 #include "kernels_mfma.h"
 #include "kernels_backward.h"
+#include "kernels_backward_mfma.h"
 
 namespace afno {
 
@@ -246,8 +247,29 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
 
 // ------------------------------------------------------------------ backward pass
 
+// the backward column pass runs the bf16 matrix-core kernel where the forward would (auto
+// path), else the size-generic one
+bool use_mfma_bwd(const Plan& pl) { return use_mfma_col(pl); }
+
 int64_t bwd_mpad(const Plan& pl) { return pl.B * pl.KW * (int64_t)col_bwd_hc((int)pl.col.H16); }
-size_t bwd_lds(const Plan& pl) { return col_bwd_lds(pl.col); }
+
+size_t bwd_lds(const Plan& pl) {
+  if (use_mfma_bwd(pl)) {
+    const int hp = mfma_col_hp(pl.H);
+#define AFNO_CASE(HP_, BS_) \
+    if (hp == HP_ && pl.bs == BS_) return (size_t)MfmaBwd<HP_, BS_>::kBytes;
+    AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
+  }
+  return col_bwd_lds(pl.col);
+}
+
+// workspace bytes of the prepared operands of the matrix-core backward column kernel: the
+// forward and the backward weight fragments, the DFT table and its rounding remainders
+size_t bwd_prep_bytes(const Plan& pl) {
+  if (!use_mfma_bwd(pl)) return 0;
+  return 2 * frag_bytes(pl) + 2 * mfma_tab_bytes(pl);
+}
 
 // The W-axis forward transform of x into S (no operand preparation).
 template <typename T>
@@ -262,6 +284,24 @@ static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream
   return hipGetLastError();
 }
 
+static void launch_col_bwd_mfma(const Plan& pl, const bf16* Sx, bf16* Sg, const uint4* wfwd,
+                                const uint4* wbwd, const uint4* tab, const uint4* tab_lo,
+                                const bf16* b1,
+                                const bf16* b2, bf16* modes, int64_t mpad, float* dbias,
+                                hipStream_t st) {
+  const int hp = mfma_col_hp(pl.H);
+  const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
+#define AFNO_CASE(HP_, BS_)                                                                   \
+  if (hp == HP_ && pl.bs == BS_) {                                                            \
+    hipLaunchKernelGGL((column_bwd_mfma<HP_, BS_>), grid, dim3(512), (MfmaBwd<HP_, BS_>::kBytes), \
+                       st, Sx, Sg, wfwd, wbwd, tab, tab_lo, b1, b2, (int)pl.H, (int)pl.C, (int)pl.KW,   \
+                       (int)pl.nb, (int)pl.kept_h, pl.col.lam, (int)pl.W, modes, mpad, dbias); \
+    return;                                                                                   \
+  }
+  AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
+}
+
 template <typename T>
 static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   const T* x = static_cast<const T*>(a.x);
@@ -273,8 +313,10 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   T* wt2 = wt1 + pl.nb * pl.bs * pl.bs * 2;
   T* modes = reinterpret_cast<T*>(ws + pl.bwd.modes_offset);
   float* acc = reinterpret_cast<float*>(ws + pl.bwd.acc_offset);
-  const int nb = (int)pl.nb, bs = (int)pl.bs;
+  const int nb = (int)pl.nb, bs = (int)pl.bs, nb2 = 2 * bs;
+  float* dbias = acc + (int64_t)2 * nb * nb2 * nb2;  // [2][nb][2 bs] after the weight products
   const int64_t mpad = bwd_mpad(pl);
+  const bool mfma = use_mfma_bwd(pl);
   hipError_t e = launch_row_forward<T>(pl, x, Sx, st);
   if (e == hipSuccess) e = launch_row_forward<T>(pl, g, Sg, st);
   if (e != hipSuccess) return e;
@@ -282,25 +324,50 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
                      dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
                      wt1, wt2, nb, bs);
-  const int64_t nacc = (int64_t)2 * nb * (2 * bs) * (2 * bs);
+  const int64_t nacc = (int64_t)2 * nb * nb2 * nb2 + (int64_t)2 * nb * nb2;
   hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nacc + 255) / 256, 4096)),
                      dim3(256), 0, st, acc, nacc);
-  hipLaunchKernelGGL(column_bwd_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
-                     dim3(pl.col_threads), bwd_lds(pl), st, Sx, Sg, static_cast<const T*>(a.w1),
-                     static_cast<const T*>(a.b1), static_cast<const T*>(a.w2),
-                     static_cast<const T*>(a.b2), wt1, wt2, pl.col, modes, mpad, (int)pl.W);
+  if constexpr (sizeof(T) == 2) {
+    if (mfma) {
+      typedef typename FragWord<T>::type Word;
+      Word* wfwd = reinterpret_cast<Word*>(ws + pl.bwd.prep_offset);
+      Word* wbwd = reinterpret_cast<Word*>(ws + pl.bwd.prep_offset + frag_bytes(pl));
+      uint4* tab = reinterpret_cast<uint4*>(ws + pl.bwd.prep_offset + 2 * frag_bytes(pl));
+      uint4* tab_lo = reinterpret_cast<uint4*>(ws + pl.bwd.prep_offset + 2 * frag_bytes(pl) +
+                                               mfma_tab_bytes(pl));
+      const int hp = mfma_col_hp(pl.H);
+      const int64_t ntab = (int64_t)mfma_tab_bytes(pl) / 16;
+      hipLaunchKernelGGL(prep_dft_lo_kernel, dim3((unsigned)((ntab + 255) / 256)), dim3(256), 0, st,
+                         tab_lo, (int)pl.H, hp, ntab);
+      PrepJob<T> pf{static_cast<const T*>(a.w1), static_cast<const T*>(a.w2), wfwd, tab, nb, bs,
+                    (int)pl.H, hp, 0};
+      PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0};
+      const unsigned gf = (unsigned)std::min<int64_t>((prep_words_host(pl, true) + 255) / 256, 4096);
+      const unsigned gb = (unsigned)std::min<int64_t>((prep_words_host(pl, false) + 255) / 256, 4096);
+      hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(gf), dim3(256), 0, st, pf);
+      hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(gb), dim3(256), 0, st, pb);
+      launch_col_bwd_mfma(pl, Sx, Sg, reinterpret_cast<const uint4*>(wfwd),
+                          reinterpret_cast<const uint4*>(wbwd), tab, tab_lo,
+                          static_cast<const T*>(a.b1),
+                          static_cast<const T*>(a.b2), modes, mpad, dbias, st);
+    }
+  }
+  if (!mfma)
+    hipLaunchKernelGGL(column_bwd_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
+                       dim3(pl.col_threads), bwd_lds(pl), st, Sx, Sg, static_cast<const T*>(a.w1),
+                       static_cast<const T*>(a.b1), static_cast<const T*>(a.w2),
+                       static_cast<const T*>(a.b2), wt1, wt2, pl.col, modes, mpad, (int)pl.W,
+                       dbias);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // weight gradients: K split in chunks of whole 32-mode steps, a few per output tile
-  const int nt64 = (2 * bs + 63) / 64;
+  const int nt64 = (nb2 + 63) / 64;
   const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
   const int kchunk = (int)(((mpad + nk - 1) / nk + 31) / 32 * 32);
   const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)((mpad + kchunk - 1) / kchunk));
   hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kchunk, acc);
   hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
-                     0, st, acc, nb, bs, a.dw1, a.dw2);
-  hipLaunchKernelGGL(bias_grad_kernel<T>, dim3((unsigned)(2 * nb * 2 * bs)), dim3(256), 0, st, modes,
-                     mpad, nb, bs, a.db1, a.db2);
+                     0, st, acc, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // dx = g + C2R(Sg): the W-axis inverse with g as the residual
@@ -346,6 +413,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(column_kernel<bf16>)
   AFNO_ATTR(column_bwd_kernel<float>)
   AFNO_ATTR(column_bwd_kernel<bf16>)
+#define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_bwd_mfma<HP_, BS_>))
+  AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
   AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))

@@ -15,12 +15,14 @@
 //   dx  = g + G(dX / c_kw)                (F's transpose: C2R with unit weights)
 //   dW1 = sum over modes conj(X)^T dv,  db1 = sum dv;  dW2 = sum conj(h)^T do,  db2 = sum do
 //
-// Passes: the forward W-axis kernel on x and on g (spectra Sx, Sg); column_bwd_kernel per
-// (b, kw, block) recomputes X, h and both masks, transforms the gradient column and runs
-// the two conjugate-transposed products, writing dX's inverse back into Sg and the per-mode
-// factors X, h, do, dv to HBM mode-contiguous; wgrad_kernel reduces the weight gradients
-// over all modes on the matrix cores; row sums give the bias gradients; the forward W-axis
-// inverse kernel with g as its residual gives dx.
+// Passes: the forward W-axis kernel on x and on g (spectra Sx, Sg); a backward column kernel
+// per (b, kw, block) recomputes X, h and both masks, transforms the gradient column and runs
+// the two conjugate-transposed products, writing dX's inverse back into Sg, the per-mode
+// factors X, h, do, dv to HBM in 8-mode groups and the bias sums (db2 = sum do, db1 = sum dv)
+// by fp32 atomics; wgrad_kernel reduces the weight gradients over all modes on the matrix
+// cores; the forward W-axis inverse kernel with g as its residual gives dx.  This header
+// holds the size-generic column kernel (any dtype, H <= 192); kernels_backward_mfma.h the bf16
+// one for H <= 96 with the H transforms on the matrix cores.
 #pragma once
 #include "kernels_generic.h"
 
@@ -53,18 +55,20 @@ __global__ void __launch_bounds__(256) fill_zero_f32(float* __restrict__ p, int6
     p[t] = 0.f;
 }
 
-// Per-mode factors: four tensors [4][nb][2 bs][mpad] in T (X, h, do, dv), entry-major with the
-// modes contiguous; the column (b, kw) holds modes (b KW + kw) HC .. + HC - 1, HC = H16
-// rounded up to 32 (rows past H hold X = 0, do = dv = 0, so they add nothing to the sums);
-// mpad = B KW HC, a multiple of the bf16 product's 32-mode k-step.
+// Per-mode factors: four tensors (X, h, do, dv), each [nb][mpad / 8][2 bs][8] in T: modes in
+// groups of eight, the group's 2 bs entries consecutive, eight modes per entry contiguous (one
+// 16-byte matrix-core operand for bf16).  The column (b, kw) holds modes (b KW + kw) HC ..
+// + HC - 1, HC = H16 rounded up to 32 (rows past H hold X = 0, do = dv = 0, so they add
+// nothing to the sums); mpad = B KW HC, a multiple of the bf16 product's 32-mode k-step.
 enum { kModeX = 0, kModeH = 1, kModeDo = 2, kModeDv = 3 };
 
-// tile rows 0 .. HC - 1 of the block's 2 bs entries -> dst[e][m0 + row], 8 rows per task
+// tile rows 0 .. HC - 1 of the block's 2 bs entries -> dst groups m0 / 8 .., 8 rows per task
 // (rows past H16 are zero)
 template <typename T>
 __device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int HC, int bs,
-                                            T* dst, int64_t mpad, int64_t m0) {
+                                            T* dst, int64_t m0) {
   const int tasks = bs * (HC / 8);
+  const int nb2 = 2 * bs;
   for (int t = threadIdx.x; t < tasks; t += blockDim.x) {
     const int c = t % bs, r0 = 8 * (t / bs);
     float re[8], im[8];
@@ -74,8 +78,8 @@ __device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int
       re[i] = z.x;
       im[i] = z.y;
     }
-    T* pr = dst + (int64_t)(2 * c) * mpad + m0 + r0;
-    T* pi = pr + mpad;
+    T* pr = dst + (((m0 + r0) / 8) * nb2 + 2 * c) * 8;
+    T* pi = pr + 8;
     if constexpr (sizeof(T) == 2) {
       union { uint4 u; bf16 h[8]; } a, b;
 #pragma unroll
@@ -92,6 +96,19 @@ __device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int
         *reinterpret_cast<float4*>(pi + i) = make_float4(im[i], im[i + 1], im[i + 2], im[i + 3]);
       }
     }
+  }
+}
+
+// column sums of the tile's first `rows` rows over its 2 bs entries, added to dst (fp32
+// atomics); the block has at least 2 bs threads
+template <typename T>
+__device__ __forceinline__ void tile_col_sums(const T* tile, int ldt, int rows, int nb2,
+                                              float* dst) {
+  const int e = threadIdx.x;
+  if (e < nb2) {
+    float s = 0.f;
+    for (int r = 0; r < rows; ++r) s += ld_f(tile + r * ldt + e);
+    unsafeAtomicAdd(dst + e, s);  // device memory
   }
 }
 
@@ -156,13 +173,14 @@ __device__ __forceinline__ uint32_t mask_word(bool p0, bool p1, int lane) {
 // grid B * KW * nb (block index fastest), block 64 * max(bs / 16, 4), dynamic LDS
 // col_bwd_lds(p).  Sx: the forward spectrum of x; Sg: that of g, replaced by
 // G^-1-side gradient dX' = IDFT_H(dX) / c_kw (so that the forward C2R kernel's c_kw weights
-// give the unit-weight transpose); modes: the four per-mode factor tensors.
+// give the unit-weight transpose); modes: the four per-mode factor tensors; dbias: [2][nb][2 bs]
+// fp32 sums (layer 0 db1, layer 1 db2).
 template <typename T>
 __global__ void __launch_bounds__(kColMaxThreads)
 column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restrict__ w1,
                   const T* __restrict__ b1, const T* __restrict__ w2, const T* __restrict__ b2,
                   const T* __restrict__ wt1, const T* __restrict__ wt2, ColParams p,
-                  T* __restrict__ modes, int64_t mpad, int W) {
+                  T* __restrict__ modes, int64_t mpad, int W, float* __restrict__ dbias) {
   extern __shared__ float4 smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);
   const size_t mk_bytes = col_bwd_mask_bytes(p);
@@ -201,7 +219,7 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
   load_column<T>(tile, Sx + coff, row_stride, ldt, H, H16, bs, 1.f);
   __syncthreads();
   dft_tile<T, false>(tile, fbuf, tw, p);
-  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeX), mpad, m0);
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeX), m0);
 
   // ---- layer 1: h = relu(X W1 + b1) -> tile, mask v > 0
   if (active) block_gemm<T>(tile, ldt, w1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -227,7 +245,7 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
     }
   }
   __syncthreads();
-  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeH), mpad, m0);
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeH), m0);
 
   // ---- layer 2: only its mask |o| > lam (and the cutoff) is needed
   if (active) block_gemm<T>(tile, ldt, w2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -259,7 +277,8 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
     if (!((mk2[row * nw + (e >> 5)] >> (e & 31)) & 1u)) tile[row * ldt + e] = Store<T>::to(0.f);
   }
   __syncthreads();
-  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDo), mpad, m0);
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDo), m0);
+  tile_col_sums<T>(tile, ldt, H16, nb2, dbias + ((int64_t)p.nb + blk) * nb2);
 
   // ---- dv = (do W2^H) masked by v > 0; write dv
   if (active) block_gemm<T>(tile, ldt, wt2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -278,7 +297,8 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
     }
   }
   __syncthreads();
-  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDv), mpad, m0);
+  write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDv), m0);
+  tile_col_sums<T>(tile, ldt, H16, nb2, dbias + (int64_t)blk * nb2);
 
   // ---- dX = dv W1^H -> inverse H-DFT -> Sg column / c_kw
   if (active) block_gemm<T>(tile, ldt, wt1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -343,12 +363,14 @@ __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes,
     for (int i = 0; i < 2; ++i) {
       const int r = rv[i] ? r0 + 16 * i + l16 : 0;
       const int s = sv[i] ? s0 + 16 * i + l16 : 0;
-      if constexpr (sizeof(T) == 2) {
-        a[i] = *reinterpret_cast<const bf16x8*>(A + (int64_t)r * mpad + k + 8 * gq);
-        bfr[i] = *reinterpret_cast<const bf16x8*>(Bm + (int64_t)s * mpad + k + 8 * gq);
+      if constexpr (sizeof(T) == 2) {  // eight modes k + 8 gq .. + 7: one group
+        const int64_t grp = (k >> 3) + gq;
+        a[i] = *reinterpret_cast<const bf16x8*>(A + (grp * nb2 + r) * 8);
+        bfr[i] = *reinterpret_cast<const bf16x8*>(Bm + (grp * nb2 + s) * 8);
       } else {
-        a[i] = A[(int64_t)r * mpad + k + gq];
-        bfr[i] = Bm[(int64_t)s * mpad + k + gq];
+        const int64_t md = k + gq;
+        a[i] = A[((md >> 3) * nb2 + r) * 8 + (md & 7)];
+        bfr[i] = Bm[((md >> 3) * nb2 + s) * 8 + (md & 7)];
       }
     }
 #pragma unroll
@@ -373,12 +395,17 @@ __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes,
 
 // dW (re, im) from the real-entry products: for entries r = (i, rho), s = (j, sigma),
 // dW[i][j] = (P[(i,0)][(j,0)] + P[(i,1)][(j,1)], P[(i,0)][(j,1)] - P[(i,1)][(j,0)])
-// (conj(a) b summed); grid over 2 nb bs^2.
+// (conj(a) b summed); the bias sums [2][nb][2 bs] after the products copy to db1, db2.
+// Grid over 2 nb bs^2.
 __global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ acc_in, int nb,
                                                       int bs, float* __restrict__ dw1,
-                                                      float* __restrict__ dw2) {
+                                                      float* __restrict__ dw2,
+                                                      float* __restrict__ db1,
+                                                      float* __restrict__ db2) {
   const int nb2 = 2 * bs;
   const int64_t n = (int64_t)nb * bs * bs;
+  const int64_t nbias = (int64_t)nb * nb2;
+  const float* bias = acc_in + (int64_t)2 * nb * nb2 * nb2;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
        t += (int64_t)gridDim.x * blockDim.x) {
     const int layer = t >= n ? 1 : 0;
@@ -391,31 +418,8 @@ __global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ 
     float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
     d[0] = rr + ii;
     d[1] = ri - ir;
+    if (t < 2 * nbias) (t < nbias ? db1 : db2)[t < nbias ? t : t - nbias] = bias[t];
   }
-}
-
-// bias gradients: db[blk][j][rho] = sum over modes of B[(j, rho)][m]; one workgroup per
-// (layer, blk, entry); layer 0 sums dv (db1), layer 1 sums do (db2)
-template <typename T>
-__global__ void __launch_bounds__(256) bias_grad_kernel(const T* __restrict__ modes, int64_t mpad,
-                                                        int nb, int bs, float* __restrict__ db1,
-                                                        float* __restrict__ db2) {
-  const int nb2 = 2 * bs;
-  const int e = blockIdx.x % nb2;
-  const int blk = (blockIdx.x / nb2) % nb;
-  const int layer = blockIdx.x / (nb2 * nb);
-  const T* row = modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * nb2 * mpad +
-                 (int64_t)e * mpad;
-  float s = 0.f;
-  for (int64_t m = threadIdx.x; m < mpad; m += blockDim.x) s += ld_f(row + m);
-  __shared__ float red[256];
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) ((layer ? db2 : db1) + (int64_t)blk * nb2)[e] = red[0];
 }
 
 }  // namespace afno
