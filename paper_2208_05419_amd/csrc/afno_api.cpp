@@ -265,8 +265,7 @@ int run_backward(const Args& a, const void* gout, float* dw1, float* db1, float*
   pl.bwd.modes_offset = pl.bwd.prep_offset + up(afno::bwd_prep_bytes(pl));
   const size_t modes_bytes = (size_t)4 * a.nb * 2 * pl.bs * (size_t)afno::bwd_mpad(pl) * es;
   pl.bwd.acc_offset = pl.bwd.modes_offset + up(modes_bytes);
-  pl.bwd.bytes = pl.bwd.acc_offset + ((size_t)2 * a.nb * (2 * pl.bs) * (2 * pl.bs) +
-                                      (size_t)2 * a.nb * (2 * pl.bs)) * 4;
+  pl.bwd.bytes = pl.bwd.acc_offset + afno::bwd_acc_floats(pl) * 4;
   void* ws = nullptr;
   e = hipMallocAsync(&ws, pl.bwd.bytes, stream);
   if (e != hipSuccess) {

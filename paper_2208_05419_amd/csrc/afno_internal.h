@@ -83,6 +83,8 @@ size_t mfma_tab_bytes(const Plan& pl);
 int64_t bwd_mpad(const Plan& pl);
 size_t bwd_lds(const Plan& pl);
 size_t bwd_prep_bytes(const Plan& pl);  // prepared operands of the matrix-core backward
+size_t bwd_acc_floats(const Plan& pl);  // fp32 sums of the weight and bias gradients
+int wgrad_slab_chunks(const Plan& pl, int* kchunk);
 hipError_t launch_backward(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,

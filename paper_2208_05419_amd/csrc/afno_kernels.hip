@@ -271,6 +271,28 @@ size_t bwd_prep_bytes(const Plan& pl) {
   return 2 * frag_bytes(pl) + 2 * mfma_tab_bytes(pl);
 }
 
+// chunks of the slab weight-gradient kernel (bf16, 2 bs = 64, 128 or 192), 0 where the
+// tiled kernel runs instead; *kchunk: modes per chunk (a multiple of 32).  About two
+// workgroups per compute unit.
+int wgrad_slab_chunks(const Plan& pl, int* kchunk) {
+  const int64_t nb2 = 2 * pl.bs;
+  if (pl.dtype != 1 || (nb2 != 64 && nb2 != 128 && nb2 != 192)) return 0;
+  const int64_t mpad = bwd_mpad(pl);
+  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(64, 512 / (2 * pl.nb)));
+  const int64_t kc = std::max<int64_t>(32, ((mpad + want - 1) / want + 31) / 32 * 32);
+  *kchunk = (int)kc;
+  return (int)((mpad + kc - 1) / kc);
+}
+
+// floats of the backward's fp32 sums: the weight products' (per chunk for the slab kernel)
+// and the bias sums
+size_t bwd_acc_floats(const Plan& pl) {
+  int kc = 0;
+  const int ns = wgrad_slab_chunks(pl, &kc);
+  const size_t nb2 = 2 * (size_t)pl.bs;
+  return (size_t)(ns > 0 ? ns : 1) * 2 * pl.nb * nb2 * nb2 + 2 * (size_t)pl.nb * nb2;
+}
+
 // The W-axis forward transform of x into S (no operand preparation).
 template <typename T>
 static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream_t st) {
@@ -314,7 +336,12 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   T* modes = reinterpret_cast<T*>(ws + pl.bwd.modes_offset);
   float* acc = reinterpret_cast<float*>(ws + pl.bwd.acc_offset);
   const int nb = (int)pl.nb, bs = (int)pl.bs, nb2 = 2 * bs;
-  float* dbias = acc + (int64_t)2 * nb * nb2 * nb2;  // [2][nb][2 bs] after the weight products
+  int kchunk = 0;
+  const int nslab = wgrad_slab_chunks(pl, &kchunk);
+  // the weight products' sums ([2][nb][2 bs][2 bs], or per chunk for the slab kernel), then
+  // the bias sums [2][nb][2 bs]
+  const int64_t nprod = (int64_t)(nslab > 0 ? nslab : 1) * 2 * nb * nb2 * nb2;
+  float* dbias = acc + nprod;
   const int64_t mpad = bwd_mpad(pl);
   const bool mfma = use_mfma_bwd(pl);
   hipError_t e = launch_row_forward<T>(pl, x, Sx, st);
@@ -324,9 +351,11 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
                      dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
                      wt1, wt2, nb, bs);
-  const int64_t nacc = (int64_t)2 * nb * nb2 * nb2 + (int64_t)2 * nb * nb2;
-  hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nacc + 255) / 256, 4096)),
-                     dim3(256), 0, st, acc, nacc);
+  // cleared: the bias sums, and the products' sums where atomics accumulate them
+  float* zero_from = nslab > 0 ? dbias : acc;
+  const int64_t nzero = (int64_t)2 * nb * nb2 + (nslab > 0 ? 0 : nprod);
+  hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
+                     dim3(256), 0, st, zero_from, nzero);
   if constexpr (sizeof(T) == 2) {
     if (mfma) {
       typedef typename FragWord<T>::type Word;
@@ -360,14 +389,30 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
                        dbias);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // weight gradients: K split in chunks of whole 32-mode steps, a few per output tile
-  const int nt64 = (nb2 + 63) / 64;
-  const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
-  const int kchunk = (int)(((mpad + nk - 1) / nk + 31) / 32 * 32);
-  const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)((mpad + kchunk - 1) / kchunk));
-  hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kchunk, acc);
-  hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
-                     0, st, acc, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
+  // weight gradients over all modes
+  if (nslab > 0) {
+    const dim3 sgrid((unsigned)(2 * nb * nslab));
+    if (nb2 == 64)
+      hipLaunchKernelGGL(wgrad_slab<64>, sgrid, dim3(512), 256 * 64, st,
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+    else if (nb2 == 128)
+      hipLaunchKernelGGL(wgrad_slab<128>, sgrid, dim3(512), 256 * 128, st,
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+    else
+      hipLaunchKernelGGL(wgrad_slab<192>, sgrid, dim3(512), 256 * 192, st,
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+    hipLaunchKernelGGL(wgrad_finalize_parts, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
+                       dim3(256), 0, st, acc, nslab, dbias, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
+  } else {
+    // 64 x 64 output tiles, K split in chunks of whole 32-mode steps, fp32 atomics
+    const int nt64 = (nb2 + 63) / 64;
+    const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
+    const int kc = (int)(((mpad + nk - 1) / nk + 31) / 32 * 32);
+    const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)((mpad + kc - 1) / kc));
+    hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kc, acc);
+    hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
+                       0, st, acc, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // dx = g + C2R(Sg): the W-axis inverse with g as the residual
@@ -413,6 +458,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(column_kernel<bf16>)
   AFNO_ATTR(column_bwd_kernel<float>)
   AFNO_ATTR(column_bwd_kernel<bf16>)
+  AFNO_ATTR(wgrad_slab<64>)
+  AFNO_ATTR(wgrad_slab<128>)
+  AFNO_ATTR(wgrad_slab<192>)
 #define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_bwd_mfma<HP_, BS_>))
   AFNO_MFMA_COL_LIST(AFNO_CASE)
 #undef AFNO_CASE

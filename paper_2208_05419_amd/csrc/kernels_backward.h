@@ -25,6 +25,7 @@
 // one for H <= 96 with the H transforms on the matrix cores.
 #pragma once
 #include "kernels_generic.h"
+#include "kernels_mfma.h"
 
 namespace afno {
 
@@ -415,6 +416,129 @@ __global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ 
     const float* P = acc_in + ((int64_t)layer * nb + k) * nb2 * nb2;
     const float rr = P[(2 * i) * nb2 + 2 * j], ii = P[(2 * i + 1) * nb2 + 2 * j + 1];
     const float ri = P[(2 * i) * nb2 + 2 * j + 1], ir = P[(2 * i + 1) * nb2 + 2 * j];
+    float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
+    d[0] = rr + ii;
+    d[1] = ri - ir;
+    if (t < 2 * nbias) (t < nbias ? db1 : db2)[t < nbias ? t : t - nbias] = bias[t];
+  }
+}
+
+// bf16 weight-gradient products for 2 bs = NB2 a multiple of 64: one workgroup per (layer,
+// block, mode chunk) computes the chunk's whole NB2 x NB2 product, so each per-mode operand is
+// read from HBM once.  Per 32-mode k-step the two operand slabs (4 mode groups x NB2 entries x
+// 16 bytes each) stream through LDS, double buffered, the next step's global loads in flight
+// during the current step's products; 8 waves as 4 x 2, each (NB2 / 64) x (NB2 / 32) output
+// tiles of 16 x 16.  The chunk's sums go to part[chunk][layer][blk][r][s] (plain stores).
+// grid 2 nb nchunk (layer, block, chunk with block fastest), 512 threads, dynamic LDS
+// 4 * 4 * NB2 * 16 bytes.
+template <int NB2>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
+wgrad_slab(const bf16* __restrict__ modes, int64_t mpad,
+                                                  int nb, int kchunk, float* __restrict__ part) {
+  constexpr int RT = NB2 / 64, CT = NB2 / 32;
+  constexpr int SLAB = 4 * NB2;                   // 16-byte words per operand and k-step
+  constexpr int LW = 2 * SLAB / 512;              // words each thread moves per k-step
+  static_assert(2 * SLAB % 512 == 0, "whole words per thread");
+  extern __shared__ uint4 slab_lds[];             // [2 buffers][2 operands][SLAB]
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, gq = lane >> 4;
+  const int wave = tid >> 6, wr = wave >> 1, wc = wave & 1;
+  int g = blockIdx.x;
+  const int blk = g % nb;
+  g /= nb;
+  const int layer = g & 1;
+  const int chunk = g >> 1;
+  const uint4* A = reinterpret_cast<const uint4*>(
+      modes + ((int64_t)(layer ? kModeH : kModeX) * nb + blk) * NB2 * mpad);
+  const uint4* Bm = reinterpret_cast<const uint4*>(
+      modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * NB2 * mpad);
+  const int64_t k0 = (int64_t)chunk * kchunk;
+  const int64_t k1 = k0 + kchunk < mpad ? k0 + kchunk : mpad;
+  const int steps = (int)((k1 - k0) / 32);
+
+  // word w of a k-step: operand w / SLAB, mode group (w % SLAB) / NB2, entry w % NB2
+  const uint4* src[LW];
+  int64_t soff[LW];
+#pragma unroll
+  for (int i = 0; i < LW; ++i) {
+    const int w = tid + 512 * i;
+    const int op = w / SLAB, idx = w - op * SLAB;
+    const int q = idx / NB2, r = idx - q * NB2;
+    src[i] = op ? Bm : A;
+    soff[i] = (k0 >> 3) * NB2 + q * NB2 + r;
+  }
+  f32x4 acc[RT][CT];
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < CT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (steps > 0) {
+    uint4 rv[LW];
+#pragma unroll
+    for (int i = 0; i < LW; ++i) rv[i] = src[i][soff[i]];
+#pragma unroll
+    for (int i = 0; i < LW; ++i) slab_lds[tid + 512 * i] = rv[i];
+  }
+  __syncthreads();
+  for (int s = 0; s < steps; ++s) {
+    const int buf = s & 1;
+    // the next k-step's words (4 mode groups further on; the last step reloads its own, so
+    // that loads and stores stay unconditional and the words stay in registers)
+    const int64_t nxt = (int64_t)(s + 1 < steps ? s + 1 : s) * 4 * NB2;
+    uint4 nv[LW];
+#pragma unroll
+    for (int i = 0; i < LW; ++i) nv[i] = src[i][soff[i] + nxt];
+    const uint4* LA = slab_lds + buf * 2 * SLAB + gq * NB2 + l16;
+    const uint4* LB = LA + SLAB;
+    uint4 a[RT], b[CT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i) a[i] = LA[16 * (wr * RT + i)];
+#pragma unroll
+    for (int j = 0; j < CT; ++j) b[j] = LB[16 * (wc * CT + j)];
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < CT; ++j) acc[i][j] = mma_bf16(a[i], b[j], acc[i][j]);
+#pragma unroll
+    for (int i = 0; i < LW; ++i) slab_lds[(buf ^ 1) * 2 * SLAB + tid + 512 * i] = nv[i];
+    __syncthreads();
+  }
+  float* out = part + (((int64_t)chunk * 2 + layer) * nb + blk) * NB2 * NB2;
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < CT; ++j) {
+      const int col = 16 * (wc * CT + j) + l16;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) out[(16 * (wr * RT + i) + 4 * gq + q) * NB2 + col] = acc[i][j][q];
+    }
+}
+
+// dW (re, im) from wgrad_slab's chunk sums (summed over the chunks here), and the bias sums
+// [2][nb][2 bs] copied to db1, db2.  Grid over 2 nb bs^2.
+__global__ void __launch_bounds__(256) wgrad_finalize_parts(const float* __restrict__ part,
+                                                            int nchunk, const float* __restrict__ bias,
+                                                            int nb, int bs, float* __restrict__ dw1,
+                                                            float* __restrict__ dw2,
+                                                            float* __restrict__ db1,
+                                                            float* __restrict__ db2) {
+  const int nb2 = 2 * bs;
+  const int64_t n = (int64_t)nb * bs * bs;
+  const int64_t nbias = (int64_t)nb * nb2;
+  const int64_t cstride = (int64_t)2 * nb * nb2 * nb2;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int layer = t >= n ? 1 : 0;
+    const int64_t u = t - layer * n;
+    const int64_t k = u / ((int64_t)bs * bs);
+    const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
+    const float* P = part + ((int64_t)layer * nb + k) * nb2 * nb2;
+    float rr = 0.f, ii = 0.f, ri = 0.f, ir = 0.f;
+    for (int c = 0; c < nchunk; ++c, P += cstride) {
+      rr += P[(2 * i) * nb2 + 2 * j];
+      ii += P[(2 * i + 1) * nb2 + 2 * j + 1];
+      ri += P[(2 * i) * nb2 + 2 * j + 1];
+      ir += P[(2 * i + 1) * nb2 + 2 * j];
+    }
     float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
     d[0] = rr + ii;
     d[1] = ri - ir;
