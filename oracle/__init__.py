@@ -43,10 +43,15 @@ def _load():
                                   _l, _l, _dp]
     lib.orc_filter_forward.argtypes = [_dp, _dp, _dp, _dp, _dp, _l, _l, _l, _l, _l,
                                        ctypes.c_double, ctypes.c_double, _dp, _dp, _dp, _dp]
+    lib.orc_block_mlp_h.argtypes = [_dp, _dp, _dp, _dp, _dp, _l, _l, _l, _l, _l, _l,
+                                    ctypes.c_double, _l, _l, _dp]
+    lib.orc_filter_forward_h.argtypes = [_dp, _dp, _dp, _dp, _dp, _l, _l, _l, _l, _l, _l,
+                                         ctypes.c_double, ctypes.c_double, _dp, _dp, _dp, _dp]
     lib.orc_dft2_bruteforce.argtypes = [_dp, _l, _l, _l, _l, _dp]
     lib.orc_idft2_bruteforce.argtypes = [_dp, _l, _l, _l, _l, _dp]
     for f in ("orc_dft_w_r2c", "orc_dft_h", "orc_dft_w_c2r", "orc_block_mlp",
-              "orc_filter_forward", "orc_dft2_bruteforce", "orc_idft2_bruteforce",
+              "orc_filter_forward", "orc_block_mlp_h", "orc_filter_forward_h",
+              "orc_dft2_bruteforce", "orc_idft2_bruteforce",
               "orc_num_threads"):
         getattr(lib, f).restype = ctypes.c_int
     lib.orc_num_threads.argtypes = []
@@ -127,25 +132,40 @@ def irfft2(Y, W: int) -> np.ndarray:
     return y
 
 
+def _hidden(w1, b1, w2, b2, num_blocks: int, C: int) -> int:
+    """Hidden units per block, from the weights' shapes: w1 [nb][bs][hs][2], b1 [nb][hs][2],
+    w2 [nb][hs][bs][2], b2 [nb][bs][2] (hs = bs is the filter's default)."""
+    bs = C // num_blocks
+    hs = int(np.shape(w1)[2])
+    if (np.shape(w1) != (num_blocks, bs, hs, 2) or np.shape(b1) != (num_blocks, hs, 2)
+            or np.shape(w2) != (num_blocks, hs, bs, 2) or np.shape(b2) != (num_blocks, bs, 2)):
+        raise ValueError("weight shapes do not match num_blocks, the block size and a hidden size")
+    return hs
+
+
 def block_mlp(X, w1, b1, w2, b2, num_blocks: int, lam: float, keep: float, W: int) -> np.ndarray:
-    """MLP + softshrink + cutoff on a spectrum [B,H,Wm,C] complex; returns the same shape."""
+    """MLP + softshrink + cutoff on a spectrum [B,H,Wm,C] complex; returns the same shape.
+    The hidden size is w1's third dimension."""
     X = np.asarray(X)
     B, H, Wm, C = X.shape
+    hs = _hidden(w1, b1, w2, b2, num_blocks, C)
     kept_h, kept_w = keep_counts(H, W, keep)
     s = _f64(np.stack([X.real, X.imag], axis=-1))
     y = np.empty_like(s)
-    _check(_load().orc_block_mlp(_ptr(s), _ptr(_f64(w1)), _ptr(_f64(b1)), _ptr(_f64(w2)),
-                                 _ptr(_f64(b2)), B, H, Wm, C, num_blocks, float(lam),
-                                 kept_h, kept_w, _ptr(y)), "block_mlp")
+    _check(_load().orc_block_mlp_h(_ptr(s), _ptr(_f64(w1)), _ptr(_f64(b1)), _ptr(_f64(w2)),
+                                   _ptr(_f64(b2)), B, H, Wm, C, num_blocks, hs, float(lam),
+                                   kept_h, kept_w, _ptr(y)), "block_mlp")
     return y[..., 0] + 1j * y[..., 1]
 
 
 def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep: float,
                    stages: bool = False):
-    """out = x + filter(x) in float64.  With stages=True also returns a dict holding
-    'spec_fwd', 'spec_mlp' (complex [B,H,Wm,C]) and 'delta' ([B,H,W,C])."""
+    """out = x + filter(x) in float64 (hidden size: w1's third dimension).  With stages=True
+    also returns a dict holding 'spec_fwd', 'spec_mlp' (complex [B,H,Wm,C]) and 'delta'
+    ([B,H,W,C])."""
     x = _f64(x)
     B, H, W, C = x.shape
+    hs = _hidden(w1, b1, w2, b2, num_blocks, C)
     Wm = W // 2 + 1
     lam = float(np.float32(lam))
     keep = float(np.float32(keep))
@@ -153,9 +173,9 @@ def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep: float,
     sf = np.empty((B, H, Wm, C, 2)) if stages else None
     sm = np.empty((B, H, Wm, C, 2)) if stages else None
     de = np.empty_like(x) if stages else None
-    _check(_load().orc_filter_forward(_ptr(x), _ptr(_f64(w1)), _ptr(_f64(b1)), _ptr(_f64(w2)),
-                                      _ptr(_f64(b2)), B, H, W, C, num_blocks, lam, keep,
-                                      _ptr(out), _ptr(sf), _ptr(sm), _ptr(de)), "filter_forward")
+    _check(_load().orc_filter_forward_h(_ptr(x), _ptr(_f64(w1)), _ptr(_f64(b1)), _ptr(_f64(w2)),
+                                        _ptr(_f64(b2)), B, H, W, C, num_blocks, hs, lam, keep,
+                                        _ptr(out), _ptr(sf), _ptr(sm), _ptr(de)), "filter_forward")
     if not stages:
         return out
     return out, {"spec_fwd": sf[..., 0] + 1j * sf[..., 1],

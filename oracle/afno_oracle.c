@@ -164,17 +164,18 @@ int orc_dft_w_c2r(const double* Y1, long B, long H, long W, long C, double* y) {
 
 /* Step 2: the block-diagonal complex two-layer MLP applied to every mode, then
  * softshrink, then the hard mode cutoff.
- * For a kept mode (kh, kw) and block k, with X the mode's bs input channels of block k:
+ * For a kept mode (kh, kw) and block k, with X the mode's bs input channels of block k and
+ * hs hidden units per block (w1 [nb][bs][hs], b1 [nb][hs], w2 [nb][hs][bs], b2 [nb][bs]):
  *   v[j] = b1[k][j] + sum_i X[i] * w1[k][i][j]          (true complex products)
  *   h[j] = ReLU(Re v[j]) + i * ReLU(Im v[j])            (parts independently)
  *   o[i] = b2[k][i] + sum_j h[j] * w2[k][j][i]
  *   Y[i] = S(Re o[i]) + i * S(Im o[i]),  S(v) = v - lam (v > lam), v + lam (v < -lam), else 0.
  * A mode outside the cutoff gets Y = 0. */
-int orc_block_mlp(const double* X, const double* w1, const double* b1, const double* w2,
-                  const double* b2, long B, long H, long Wm, long C, long nb, double lam,
-                  long kept_h, long kept_w, double* Y) {
-    if (B < 0 || H <= 0 || Wm <= 0 || C <= 0 || nb <= 0 || C % nb != 0) return -1;
-    long bs = C / nb, hs = bs;
+int orc_block_mlp_h(const double* X, const double* w1, const double* b1, const double* w2,
+                    const double* b2, long B, long H, long Wm, long C, long nb, long hs,
+                    double lam, long kept_h, long kept_w, double* Y) {
+    if (B < 0 || H <= 0 || Wm <= 0 || C <= 0 || nb <= 0 || C % nb != 0 || hs <= 0) return -1;
+    long bs = C / nb;
 #pragma omp parallel
     {
         double* hid = (double*)malloc(sizeof(double) * 2 * (size_t)hs);
@@ -226,17 +227,25 @@ int orc_block_mlp(const double* X, const double* w1, const double* b1, const dou
     return 0;
 }
 
+/* The block MLP with hidden size equal to the block size. */
+int orc_block_mlp(const double* X, const double* w1, const double* b1, const double* w2,
+                  const double* b2, long B, long H, long Wm, long C, long nb, double lam,
+                  long kept_h, long kept_w, double* Y) {
+    if (nb <= 0 || C % nb != 0) return -1;
+    return orc_block_mlp_h(X, w1, b1, w2, b2, B, H, Wm, C, nb, C / nb, lam, kept_h, kept_w, Y);
+}
+
 /* The whole filter: out = x + irfft2(MLP(rfft2(x))), axis order W then H forward,
  * H then W inverse.  Optional stage outputs (NULL to skip):
  *   spec_fwd [B][H][Wm][C][2]  the forward spectrum (after both axes);
  *   spec_mlp [B][H][Wm][C][2]  the spectrum after the MLP, softshrink and cutoff;
  *   delta    [B][H][W][C]      the filter output y = out - x before the residual add.
  * Samples are processed one at a time to bound memory. */
-int orc_filter_forward(const double* x, const double* w1, const double* b1, const double* w2,
-                       const double* b2, long B, long H, long W, long C, long nb, double lam,
-                       double keep, double* out, double* spec_fwd, double* spec_mlp,
-                       double* delta) {
-    if (B < 0 || H <= 0 || W <= 0 || C <= 0 || nb <= 0 || C % nb != 0) return -1;
+int orc_filter_forward_h(const double* x, const double* w1, const double* b1, const double* w2,
+                         const double* b2, long B, long H, long W, long C, long nb, long hs,
+                         double lam, double keep, double* out, double* spec_fwd,
+                         double* spec_mlp, double* delta) {
+    if (B < 0 || H <= 0 || W <= 0 || C <= 0 || nb <= 0 || C % nb != 0 || hs <= 0) return -1;
     if (!(lam >= 0.0) || !(keep > 0.0 && keep <= 1.0)) return -1;
     long Wm = W / 2 + 1, kept_h, kept_w;
     orc_keep_counts(H, W, keep, &kept_h, &kept_w);
@@ -251,7 +260,7 @@ int orc_filter_forward(const double* x, const double* w1, const double* b1, cons
         rc |= orc_dft_w_r2c(xb, 1, H, W, C, s1);
         rc |= orc_dft_h(s1, 1, H, Wm, C, -1, s2);
         if (spec_fwd) memcpy(spec_fwd + (size_t)b * nspec, s2, sizeof(double) * nspec);
-        rc |= orc_block_mlp(s2, w1, b1, w2, b2, 1, H, Wm, C, nb, lam, kept_h, kept_w, s1);
+        rc |= orc_block_mlp_h(s2, w1, b1, w2, b2, 1, H, Wm, C, nb, hs, lam, kept_h, kept_w, s1);
         if (spec_mlp) memcpy(spec_mlp + (size_t)b * nspec, s1, sizeof(double) * nspec);
         rc |= orc_dft_h(s1, 1, H, Wm, C, +1, s2);
         rc |= orc_dft_w_c2r(s2, 1, H, W, C, y);
@@ -261,6 +270,16 @@ int orc_filter_forward(const double* x, const double* w1, const double* b1, cons
     }
     free(s1); free(s2); free(y);
     return rc;
+}
+
+/* The whole filter with hidden size equal to the block size. */
+int orc_filter_forward(const double* x, const double* w1, const double* b1, const double* w2,
+                       const double* b2, long B, long H, long W, long C, long nb, double lam,
+                       double keep, double* out, double* spec_fwd, double* spec_mlp,
+                       double* delta) {
+    if (nb <= 0 || C % nb != 0) return -1;
+    return orc_filter_forward_h(x, w1, b1, w2, b2, B, H, W, C, nb, C / nb, lam, keep, out,
+                                spec_fwd, spec_mlp, delta);
 }
 
 /* Brute-force 2-D DFT of real input, one sum over all (h, w) per output bin

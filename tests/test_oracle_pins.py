@@ -350,3 +350,59 @@ def test_golden_tiny_fixture():
     out = oracle.filter_forward(arr["x"], arr["w1"], arr["b1"], arr["w2"], arr["b2"],
                                 g["num_blocks"], g["lam"], g["keep"])
     assert np.max(np.abs(out - np.array(g["out"]))) < 1e-12
+
+
+# ---------------------------------------------------------------- hidden size != block size
+
+
+@pytest.mark.parametrize("hs", [8, 2, 12])
+def test_linear_regime_hidden_size(hs):
+    """Hidden size hs != bs (w1 [nb][bs][hs], w2 [nb][hs][bs]): with real weights and ReLU
+    inactive the filter is out = x + x_blk @ (A @ Bm) per token, A bs x hs, Bm hs x bs."""
+    nb, bs, H, W = 2, 4, 6, 8
+    A = _rand(nb, bs, hs) * 0.2
+    Bm = _rand(nb, hs, bs) * 0.2
+    x = _rand(1, H, W, nb * bs)
+    out = oracle.filter_forward(x, *_linear_regime(A.astype(complex), Bm.astype(complex), 1e3),
+                                nb, 0.0, 1.0)
+    expect = x.copy()
+    for k in range(nb):
+        sl = slice(k * bs, (k + 1) * bs)
+        expect[..., sl] += x[..., sl] @ (A[k] @ Bm[k])
+    assert np.max(np.abs(out - expect)) < 1e-9
+
+
+def test_hidden_units_with_zero_input_weights_drop_out():
+    """Hidden units whose layer-1 weights and bias are zero stay at ReLU(0) = 0, so their
+    layer-2 rows (set to non-zero values here) contribute nothing: an hs = 2 bs MLP whose
+    second half is such units equals the hs = bs MLP of the first half, exactly."""
+    nb, bs, H, W = 2, 4, 6, 10
+    w1 = _rand(nb, bs, bs, 2) * 0.3
+    b1 = _rand(nb, bs, 2) * 0.3
+    w2 = _rand(nb, bs, bs, 2) * 0.3
+    b2 = _rand(nb, bs, 2) * 0.3
+    w1p = np.concatenate([w1, np.zeros((nb, bs, bs, 2))], axis=2)
+    b1p = np.concatenate([b1, np.zeros((nb, bs, 2))], axis=1)
+    w2p = np.concatenate([w2, _rand(nb, bs, bs, 2)], axis=1)
+    x = _rand(2, H, W, nb * bs)
+    ref = oracle.filter_forward(x, w1, b1, w2, b2, nb, 0.01, 0.8)
+    out = oracle.filter_forward(x, w1p, b1p, w2p, b2, nb, 0.01, 0.8)
+    assert np.array_equal(out, ref)
+
+
+def test_hidden_unit_permutation_invariance():
+    """Permuting the hidden units (w1 columns, b1 entries, w2 rows together) leaves the
+    filter unchanged up to summation order."""
+    nb, bs, hs, H, W = 2, 4, 10, 6, 8
+    w1 = _rand(nb, bs, hs, 2) * 0.3
+    b1 = _rand(nb, hs, 2) * 0.3
+    w2 = _rand(nb, hs, bs, 2) * 0.3
+    b2 = _rand(nb, bs, 2) * 0.3
+    perm = RNG.permutation(hs)
+    x = _rand(1, H, W, nb * bs)
+    a = oracle.filter_forward(x, w1, b1, w2, b2, nb, 0.01, 1.0)
+    b = oracle.filter_forward(x, w1[:, :, perm], b1[:, perm], w2[:, perm], b2, nb, 0.01, 1.0)
+    assert np.max(np.abs(a - b)) < 1e-12
+    # and a mismatched hidden size is rejected
+    with pytest.raises(ValueError):
+        oracle.filter_forward(x, w1, b1[:, :hs - 1], w2, b2, nb, 0.01, 1.0)
