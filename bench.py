@@ -41,9 +41,10 @@ FP32_PEAK_TFLOPS = 157.3       # fp32 matrix
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_afno90x180_c768_nb8_bf16_b4.json")
 PREWARM_S = 0.3                # untimed sustained run before the counted warm-up (clock ramp)
 # timed after the headline for context: fp32 at the headline grid, the 180 x 360 grid with 8
-# blocks of 128, and the paper's own 180 x 360 filter with 32 blocks of 32
+# blocks of 128, the paper's own 180 x 360 filter with 32 blocks of 32, and the headline grid
+# with 192 hidden units per block of 96 (hidden-size factor 2)
 OTHER_WORKLOADS = ("afno90x180_c768_nb8_fp32", "afno180x360_c1024_nb8_bf16",
-                   "afno180x360_c1024_nb32_bf16")
+                   "afno180x360_c1024_nb32_bf16", "afno90x180_c768_nb8_hs192_bf16_b4")
 # HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
 # sha256 of the kernel sources it was measured on (null once the kernels change)
 
@@ -60,15 +61,15 @@ def kernel_source_hash() -> str:
 def algorithmic_work(wl, es: int):
     """Per-launch algorithmic bytes and FLOPs of each kernel (minimum traffic of each
     standalone pass: read its input once, write its output once)."""
-    B, H, W, C, bs = wl.B, wl.H, wl.W, wl.C, wl.bs
+    B, H, W, C, bs, hs = wl.B, wl.H, wl.W, wl.C, wl.bs, wl.hs
     kept_h = int((H // 2 + 1) * wl.keep)
     kw = int((W // 2 + 1) * wl.keep)
     rows_kept = sum(1 for r in range(H) if abs(r if r <= H // 2 else r - H) < kept_h)
     x_bytes = B * H * W * C * es
     s_bytes = B * H * kw * C * 2 * es           # spectrum workspace, complex in dtype
-    flops = 16 * C * bs * B * rows_kept * kw     # two complex GEMMs, 8 real FLOP per complex MAC
+    flops = 16 * C * hs * B * rows_kept * kw     # two complex GEMMs, 8 real FLOP per complex MAC
     nb = wl.num_blocks
-    w_bytes = 2 * nb * bs * bs * 2 * es          # w1, w2 read
+    w_bytes = 2 * nb * bs * hs * 2 * es          # w1, w2 read
     frag_bytes = nb * 2 * (2 * bs) ** 2 * es     # both layers real-ified, fragment order
     hp = 32 if H <= 32 else (64 if H <= 64 else 96)
     tab_bytes = 2 * hp * hp * 2 if es == 2 and H <= 96 else 0  # bf16 DFT table

@@ -85,6 +85,22 @@ int afno_filter_forward(const void* x, const void* w1, const void* b1, const voi
                         void* out, hipStream_t stream);
 
 /*
+ * afno_filter_forward_hidden -- the same filter with `hidden` hidden units per block in
+ * the block MLP (the AFNO layer's hidden-size factor: hidden = factor * bs; the paper's
+ * filter, "Model Innovations", uses hidden = bs, which afno_filter_forward assumes).
+ *   w1 [nb][bs][hidden][2], b1 [nb][hidden][2], w2 [nb][hidden][bs][2], b2 [nb][bs][2]
+ *   hidden > 0 (AFNO_ERR_INVALID_ARG otherwise); a multiple of 16 and <= 256, and the
+ *   column's hidden layer (H x hidden complex values) must fit in LDS beside the column
+ *   tile (AFNO_ERR_UNSUPPORTED otherwise).  hidden == bs runs exactly afno_filter_forward.
+ * Other arguments, ownership and errors as afno_filter_forward.  hidden != bs runs the
+ * size-generic column kernel.
+ */
+int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, const void* w2,
+                               const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                               int64_t num_blocks, int64_t hidden, float lambda,
+                               float keep_fraction, int dtype, void* out, hipStream_t stream);
+
+/*
  * afno_filter_stage -- diagnostic entry point: runs the filter's kernels up to a stage
  * and writes that stage's result in float32, for per-stage parity checks.
  *   stage AFNO_STAGE_SPECTRUM  dst [B][H][Wm][C][2] float32: the forward spectrum X

@@ -27,7 +27,7 @@ AFNO_PATH_AUTO = 0
 AFNO_PATH_GENERIC = 1
 AFNO_PATH_VALU_DFT = 2
 
-EXPORTED = ("afno_filter_forward", "afno_filter_stage", "afno_filter_backward", "afno_profile_begin",
+EXPORTED = ("afno_filter_forward", "afno_filter_forward_hidden", "afno_filter_stage", "afno_filter_backward", "afno_profile_begin",
             "afno_profile_end", "afno_set_kernel_path", "afno_last_error", "afno_version")
 KERNELS = ("prep", "row_r2c", "column", "row_c2r")
 
@@ -63,6 +63,9 @@ def load_library():
     lib.afno_filter_forward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
                                         ctypes.c_int, vp, vp]
     lib.afno_filter_forward.restype = ctypes.c_int
+    lib.afno_filter_forward_hidden.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
+                                               f32, f32, ctypes.c_int, vp, vp]
+    lib.afno_filter_forward_hidden.restype = ctypes.c_int
     lib.afno_filter_stage.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
                                       ctypes.c_int, ctypes.c_int, vp, vp]
     lib.afno_filter_stage.restype = ctypes.c_int
@@ -102,6 +105,14 @@ def afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fra
     """Raw call: pointers as ints (or None), returns the C return code."""
     return load_library().afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam,
                                               keep_fraction, dtype, out, stream)
+
+
+def afno_filter_forward_hidden(x, w1, b1, w2, b2, B, H, W, C, num_blocks, hidden, lam,
+                               keep_fraction, dtype, out, stream) -> int:
+    """Raw call with the block MLP's hidden size: pointers as ints (or None)."""
+    return load_library().afno_filter_forward_hidden(x, w1, b1, w2, b2, B, H, W, C, num_blocks,
+                                                     hidden, lam, keep_fraction, dtype, out,
+                                                     stream)
 
 
 def afno_filter_stage(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fraction, dtype,
@@ -179,15 +190,25 @@ def _stream(stream):
 def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction: float = 1.0,
                    out=None, stream=None):
     """out = x + AFNO filter(x) for x [B,H,W,C] (float32 or bfloat16 on the GPU);
-    weights w1 [nb,bs,bs,2], b1 [nb,bs,2], w2 [nb,bs,bs,2], b2 [nb,bs,2] of x's dtype.
+    weights w1 [nb,bs,hs,2], b1 [nb,hs,2], w2 [nb,hs,bs,2], b2 [nb,bs,2] of x's dtype, the
+    hidden size hs from w1 (hs = bs: afno_filter_forward, else afno_filter_forward_hidden).
     Enqueued on ``stream`` (default: torch's current stream)."""
     import torch
     B, H, W, C = x.shape
+    bs, hs = C // num_blocks, int(w1.shape[2])
+    if tuple(w1.shape) != (num_blocks, bs, hs, 2) or tuple(b1.shape) != (num_blocks, hs, 2) or \
+            tuple(w2.shape) != (num_blocks, hs, bs, 2) or tuple(b2.shape) != (num_blocks, bs, 2):
+        raise ValueError("weight shapes do not match num_blocks, the block size and a hidden size")
     if out is None:
         out = torch.empty_like(x)
-    rc = afno_filter_forward(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W, C,
-                             num_blocks, lam, keep_fraction, _dtype_code(x), _ptr(out),
-                             _stream(stream))
+    if hs == bs:
+        rc = afno_filter_forward(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W, C,
+                                 num_blocks, lam, keep_fraction, _dtype_code(x), _ptr(out),
+                                 _stream(stream))
+    else:
+        rc = afno_filter_forward_hidden(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W,
+                                        C, num_blocks, hs, lam, keep_fraction, _dtype_code(x),
+                                        _ptr(out), _stream(stream))
     _check(rc)
     return out
 

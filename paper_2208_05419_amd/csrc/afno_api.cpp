@@ -3,6 +3,7 @@
 // spectrum workspace.  Every step of the filter runs in the kernels of afno_kernels.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
@@ -61,6 +62,7 @@ struct Args {
   int dtype;
   void* out;
   size_t out_bytes;  // 0: the size of x
+  int64_t hs;        // hidden units per block; 0: the block size
 };
 
 // Validation (no HIP call) and plan construction.  Returns AFNO_OK, or an error code
@@ -79,6 +81,8 @@ int make_plan(const Args& a, afno::Plan& pl) {
 
   pl.B = a.B; pl.H = a.H; pl.W = a.W; pl.C = a.C; pl.nb = a.nb;
   pl.bs = a.C / a.nb;
+  const int64_t hs = a.hs ? a.hs : pl.bs;
+  if (hs <= 0) return fail(AFNO_ERR_INVALID_ARG, "hidden must be > 0");
   pl.dtype = a.dtype;
   // hard mode cutoff, products in double
   const int64_t Kh = a.H / 2 + 1, Wm = a.W / 2 + 1;
@@ -100,6 +104,8 @@ int make_plan(const Args& a, afno::Plan& pl) {
     return fail(AFNO_ERR_UNSUPPORTED, "H and W must be of the form 2^a 3^b 5^c");
   if (pl.bs % 16 != 0 || pl.bs > 128)
     return fail(AFNO_ERR_UNSUPPORTED, "block size C/num_blocks must be a multiple of 16 and <= 128");
+  if (hs % 16 != 0 || hs > 256)
+    return fail(AFNO_ERR_UNSUPPORTED, "hidden size must be a multiple of 16 and <= 256");
   if (a.W > 1024) return fail(AFNO_ERR_UNSUPPORTED, "W must be <= 1024");
   if (a.H > 16 * afno::kColMaxMTiles)
     return fail(AFNO_ERR_UNSUPPORTED, "H must be <= 192");
@@ -129,11 +135,18 @@ int make_plan(const Args& a, afno::Plan& pl) {
   c.C = (int)a.C; c.KW = (int)pl.KW; c.kept_h = (int)pl.kept_h;
   c.lam = a.lam;
   c.inv_sqrt_h = (float)(1.0 / std::sqrt((double)a.H));
+  c.hs = (int)hs;
   c.ldt = 2 * c.bs + (a.dtype == AFNO_DTYPE_BF16 ? 8 : 4);
+  c.ldh = 2 * c.hs + (a.dtype == AFNO_DTYPE_BF16 ? 8 : 4);
   c.chk = (c.bs % 32 == 0) ? 32 : 16;  // must divide bs
-  pl.col_threads = 64 * (c.bs / 16 > 4 ? c.bs / 16 : 4);
+  {  // waves: one per 32 real output columns of the wider layer, 4 to 8
+    const int64_t wmax = std::max<int64_t>(c.bs, c.hs) / 16;
+    pl.col_threads = 64 * (int)std::min<int64_t>(8, std::max<int64_t>(4, wmax));
+  }
   c.tile_bytes = (int)(((size_t)c.H16 * c.ldt * es + 15) / 16 * 16);
-  pl.col_lds = (size_t)c.tile_bytes + (size_t)a.H * c.chk * 8 + (size_t)a.H * 8;
+  c.htile_bytes = c.hs == c.bs ? 0 : (int)(((size_t)c.H16 * c.ldh * es + 15) / 16 * 16);
+  pl.col_lds = (size_t)c.tile_bytes + (size_t)c.htile_bytes + (size_t)a.H * c.chk * 8 +
+               (size_t)a.H * 8;
   if (pl.col_lds > (size_t)afno::kLdsBytes)
     return fail(AFNO_ERR_UNSUPPORTED, "column tile (H x block size) does not fit in LDS");
   if (!passes_fit(c.rh, pl.col_threads / c.chk, afno::kColEmax))
@@ -149,9 +162,10 @@ int make_plan(const Args& a, afno::Plan& pl) {
   // out must not overlap any input
   const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;
   const size_t ob = a.out_bytes ? a.out_bytes : xb;
-  const size_t wb = (size_t)a.nb * pl.bs * pl.bs * 2 * es, bb = (size_t)a.nb * pl.bs * 2 * es;
+  const size_t wb = (size_t)a.nb * pl.bs * hs * 2 * es, bb = (size_t)a.nb * pl.bs * 2 * es;
+  const size_t hb = (size_t)a.nb * hs * 2 * es;
   if (overlaps(a.out, ob, a.x, xb) || overlaps(a.out, ob, a.w1, wb) ||
-      overlaps(a.out, ob, a.w2, wb) || overlaps(a.out, ob, a.b1, bb) ||
+      overlaps(a.out, ob, a.w2, wb) || overlaps(a.out, ob, a.b1, hb) ||
       overlaps(a.out, ob, a.b2, bb))
     return fail(AFNO_ERR_ALIAS, "out overlaps an input");
   return AFNO_OK;
@@ -291,6 +305,16 @@ int afno_filter_forward(const void* x, const void* w1, const void* b1, const voi
                         void* out, hipStream_t stream) {
   g_last_error.clear();
   Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0};
+  return run(a, afno::kStageFull, nullptr, stream);
+}
+
+int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, const void* w2,
+                               const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                               int64_t num_blocks, int64_t hidden, float lambda,
+                               float keep_fraction, int dtype, void* out, hipStream_t stream) {
+  g_last_error.clear();
+  if (hidden <= 0) return fail(AFNO_ERR_INVALID_ARG, "hidden must be > 0");
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0, hidden};
   return run(a, afno::kStageFull, nullptr, stream);
 }
 

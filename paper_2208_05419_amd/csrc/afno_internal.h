@@ -33,7 +33,10 @@ struct RowParams {
 
 struct ColParams {
   int H, H16, bs, nb, C, KW;
+  int hs;             // hidden units per block (hs = bs: the hidden layer reuses the tile)
   int ldt;            // LDS row stride of the column tile, elements
+  int ldh;            // LDS row stride of the hidden tile (hs != bs), elements
+  int htile_bytes;    // the hidden tile (0 when hs = bs)
   int chk;            // channels per pass of the H transform
   int kept_h;
   int tile_bytes;

@@ -167,11 +167,12 @@ static int g_kernel_path = 0;
 void set_kernel_path(int path) { g_kernel_path = path; }
 
 bool use_mfma_col(const Plan& pl) {
-  return g_kernel_path == 0 && mfma_col_available(pl.dtype, pl.H, pl.bs);
+  return g_kernel_path == 0 && pl.col.hs == pl.bs && mfma_col_available(pl.dtype, pl.H, pl.bs);
 }
 
 bool use_fast_col(const Plan& pl) {
-  return g_kernel_path != 1 && !use_mfma_col(pl) && fast_col_available(pl.dtype, pl.H, pl.bs);
+  return g_kernel_path != 1 && pl.col.hs == pl.bs && !use_mfma_col(pl) &&
+         fast_col_available(pl.dtype, pl.H, pl.bs);
 }
 
 size_t frag_bytes(const Plan& pl) {

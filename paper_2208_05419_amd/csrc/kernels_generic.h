@@ -193,19 +193,25 @@ __device__ __forceinline__ void block_gemm(const T* tile, int ldt, const T* w, i
   }
 }
 
-// grid B * KW * nb, block 64 * max(bs / 16, 4).  stage: 0 full, 1 stop after the forward
-// transform, 2 stop after the MLP.
+// grid B * KW * nb, block 64 * min(8, max(max(bs, hs) / 16, 4)).  stage: 0 full, 1 stop after
+// the forward transform, 2 stop after the MLP.  hs != bs: the hidden layer (2 hs real entries
+// per row) has its own LDS tile after the column tile, and waves take its 32-column groups in
+// turn.
 template <typename T>
 __global__ void __launch_bounds__(kColMaxThreads)
 column_kernel(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__ b1,
               const T* __restrict__ w2, const T* __restrict__ b2, ColParams p, int stage) {
   extern __shared__ float4 smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);                              // H16 x ldt
-  float2* fbuf = reinterpret_cast<float2*>(reinterpret_cast<char*>(smem_raw) + p.tile_bytes);
+  T* htile = p.htile_bytes ? reinterpret_cast<T*>(reinterpret_cast<char*>(smem_raw) + p.tile_bytes)
+                           : tile;                                       // H16 x ldh
+  float2* fbuf = reinterpret_cast<float2*>(reinterpret_cast<char*>(smem_raw) + p.tile_bytes +
+                                           p.htile_bytes);
   float2* tw = fbuf + (size_t)p.H * p.chk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nthr = blockDim.x;
-  const int bs = p.bs, ldt = p.ldt, H = p.H, H16 = p.H16;
+  const int bs = p.bs, hs = p.hs, ldt = p.ldt, H = p.H, H16 = p.H16;
+  const int ldh = p.htile_bytes ? p.ldh : ldt;
 
   const int blk = blockIdx.x % p.nb;  // consecutive workgroups -> different XCDs -> blocks
   const int rest = blockIdx.x / p.nb;
@@ -251,8 +257,7 @@ column_kernel(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__
   }
 
   if (stage != 1) {
-    // ---- block MLP.  Waves own 32 real output columns (16 complex) each.
-    const int nw_mma = bs / 16;
+    // ---- block MLP.  A wave owns 32 real output columns (16 complex) at a time.
     const int mt = H16 / 16;
     uint32_t live = 0;
     for (int m = 0; m < mt; ++m) {
@@ -260,32 +265,42 @@ column_kernel(T* __restrict__ S, const T* __restrict__ w1, const T* __restrict__
       for (int r = 16 * m; r < 16 * m + 16; ++r) any |= row_kept(r, H, p.kept_h);
       live |= (any ? 1u : 0u) << m;
     }
-    const T* W1 = w1 + (int64_t)blk * bs * bs * 2;
-    const T* W2 = w2 + (int64_t)blk * bs * bs * 2;
-    const T* B1 = b1 + (int64_t)blk * bs * 2;
+    const T* W1 = w1 + (int64_t)blk * bs * hs * 2;
+    const T* W2 = w2 + (int64_t)blk * hs * bs * 2;
+    const T* B1 = b1 + (int64_t)blk * hs * 2;
     const T* B2 = b2 + (int64_t)blk * bs * 2;
-    const bool active = wave < nw_mma;
-    const int nu0 = 32 * wave + (lane & 15);  // real output column of tile 0 (tile 1: +16)
+    const int nwaves = nthr / 64;
     f32x4 acc[kColMaxMTiles][2];
 
-    if (active) block_gemm<T>(tile, ldt, W1, bs, bs, mt, live, wave, lane, acc);
-    __syncthreads();  // every wave has read the spectrum rows
-    if (active) {
-      const float bia0 = ld_f(B1 + nu0), bia1 = ld_f(B1 + nu0 + 16);
+    // layer 1: hidden groups grp = wave, wave + nwaves, ...; in place (hs = bs: one group per
+    // wave at most) the spectrum rows are read by every wave before any is overwritten
+    const int ng1 = hs / 16;
+    const int rounds = (ng1 + nwaves - 1) / nwaves;
+    for (int rd = 0; rd < rounds; ++rd) {
+      const int grp = wave + rd * nwaves;
+      const bool act = grp < ng1;
+      if (act) block_gemm<T>(tile, ldt, W1, hs, bs, mt, live, grp, lane, acc);
+      if (htile == tile) __syncthreads();
+      if (act) {
+        const int nu = 32 * grp + (lane & 15);
+        const float bia0 = ld_f(B1 + nu), bia1 = ld_f(B1 + nu + 16);
 #pragma unroll
-      for (int m = 0; m < kColMaxMTiles; ++m) {
-        if (m < mt && ((live >> m) & 1u)) {
+        for (int m = 0; m < kColMaxMTiles; ++m) {
+          if (m < mt && ((live >> m) & 1u)) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = 16 * m + 4 * (lane >> 4) + r;
-            tile[row * ldt + nu0] = Store<T>::to(fmaxf(acc[m][0][r] + bia0, 0.f));
-            tile[row * ldt + nu0 + 16] = Store<T>::to(fmaxf(acc[m][1][r] + bia1, 0.f));
+            for (int r = 0; r < 4; ++r) {
+              const int row = 16 * m + 4 * (lane >> 4) + r;
+              htile[row * ldh + nu] = Store<T>::to(fmaxf(acc[m][0][r] + bia0, 0.f));
+              htile[row * ldh + nu + 16] = Store<T>::to(fmaxf(acc[m][1][r] + bia1, 0.f));
+            }
           }
         }
       }
     }
     __syncthreads();  // hidden layer complete
-    if (active) block_gemm<T>(tile, ldt, W2, bs, bs, mt, live, wave, lane, acc);
+    const bool active = wave < bs / 16;
+    const int nu0 = 32 * wave + (lane & 15);  // real output column of tile 0 (tile 1: +16)
+    if (active) block_gemm<T>(htile, ldh, W2, bs, hs, mt, live, wave, lane, acc);
     __syncthreads();  // every wave has read the hidden rows
     if (active) {
       const float bia0 = ld_f(B2 + nu0), bia1 = ld_f(B2 + nu0 + 16);

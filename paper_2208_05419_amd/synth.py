@@ -41,6 +41,11 @@ class Workload:
     keep: float
     x_kind: str = "normal"   # "normal" | "channel_scaled" | "ensemble"
     weight_std: float = 0.02
+    hidden: int = 0          # hidden units per block; 0: the block size
+
+    @property
+    def hs(self) -> int:
+        return self.hidden or self.C // self.num_blocks
 
     @property
     def bs(self) -> int:
@@ -58,6 +63,9 @@ WORKLOADS = {
         Workload("afno180x360_c1024_nb32_bf16", 1, 180, 360, 1024, 32, "bf16", 0.01, 1.0),
         Workload("afno90x180_c768_nb8_bf16_ens100_keep0.5", 100, 90, 180, 768, 8, "bf16", 0.01,
                  0.5, "ensemble"),
+        # hidden-size factor 2 (192 hidden units per block of 96)
+        Workload("afno90x180_c768_nb8_hs192_bf16_b4", 4, 90, 180, 768, 8, "bf16", 0.01, 1.0,
+                 "channel_scaled", hidden=192),
     ]
 }
 
@@ -115,9 +123,9 @@ def make_x(wl: Workload, seed: int = 0, members=None) -> np.ndarray:
 
 def make_weights(wl: Workload, seed: int = 0) -> dict:
     """Complex block weights and biases in stored form, (re, im) as the fastest index:
-    w1 [nb][bs][hs][2], b1 [nb][hs][2], w2 [nb][hs][bs][2], b2 [nb][bs][2]; hs = bs."""
+    w1 [nb][bs][hs][2], b1 [nb][hs][2], w2 [nb][hs][bs][2], b2 [nb][bs][2]; hs = wl.hs."""
     nb, bs = wl.num_blocks, wl.bs
-    hs = bs
+    hs = wl.hs
     rng = np.random.default_rng(np.random.SeedSequence([seed, 3]))
     s = wl.weight_std
 

@@ -150,3 +150,28 @@ def test_backward_unsupported(kw):
                                 dict(db1=G + 128), dict(db2=DX)])
 def test_backward_alias(kw):
     assert call_bwd(**kw) == afno.AFNO_ERR_ALIAS
+
+
+def call_hidden(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, B=1, H=16, W=32, C=64, nb=4, hidden=32, lam=0.01,
+             keep=1.0, dtype=afno.AFNO_DTYPE_FP32, out=OUT)
+    a.update(kw)
+    return afno.afno_filter_forward_hidden(a["x"], a["w1"], a["b1"], a["w2"], a["b2"], a["B"],
+                                           a["H"], a["W"], a["C"], a["nb"], a["hidden"], a["lam"],
+                                           a["keep"], a["dtype"], a["out"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(hidden=0), dict(hidden=-16), dict(w1=None), dict(nb=3)])
+def test_hidden_invalid_arguments(kw):
+    assert call_hidden(**kw) == afno.AFNO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(hidden=24), dict(hidden=272), dict(H=180, C=256, nb=2, hidden=256)])
+def test_hidden_unsupported(kw):
+    assert call_hidden(**kw) == afno.AFNO_ERR_UNSUPPORTED
+
+
+def test_hidden_alias_covers_the_wider_weights():
+    # w1 is nb * bs * hidden * 2 * 4 = 4 * 16 * 32 * 8 = 16 KiB: out 12 KiB after w1 overlaps it
+    assert call_hidden(out=W1 + 12 * 1024) == afno.AFNO_ERR_ALIAS
+    assert call_hidden(out=B1 + 256) == afno.AFNO_ERR_ALIAS   # b1: 4 * 32 * 8 = 1 KiB

@@ -1,0 +1,78 @@
+"""GPU parity of the block MLP with a hidden size other than the block size
+(afno_filter_forward_hidden, the size-generic column kernel) against the float64 oracle,
+whose hidden size comes from the weights' shapes.
+
+Bars as the forward's: fp32 1e-4 on out and on the filter's delta out - x (out is float32,
+so out - x is exact to ~1e-6 of the delta's scale); bf16 2e-2 on out, with weights of std 0.1
+so that the filter's delta is of the order of x itself and out shows it (with the default
+0.02 the bf16 rounding of out would hide the filter)."""
+import numpy as np
+import pytest
+
+import paper_2208_05419_amd as afno
+from paper_2208_05419_amd import synth
+from gpu_util import dev_weights, max_rel, oracle_run, say, to_dev, to_f64
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    afno.load_library()
+
+
+CASES = [
+    # B, H, W, C, nb, hidden, dtype, lam, keep, weight_std
+    (1, 16, 32, 64, 4, 32, "fp32", 0.01, 1.0, 0.02),
+    (2, 12, 20, 64, 2, 64, "fp32", 0.01, 0.7, 0.02),
+    (1, 30, 24, 128, 2, 32, "fp32", 0.01, 1.0, 0.02),      # hidden < block size
+    (1, 45, 16, 128, 2, 128, "fp32", 0.02, 1.0, 0.02),
+    (1, 20, 12, 64, 1, 256, "fp32", 0.01, 1.0, 0.02),      # eight waves, four groups each
+    (1, 90, 180, 768, 8, 192, "bf16", 0.01, 1.0, 0.1),     # hidden factor 2 at 90 x 180
+    (2, 25, 30, 96, 2, 96, "bf16", 0.01, 0.6, 0.1),
+    (1, 1, 2, 32, 1, 64, "bf16", 0.01, 1.0, 0.1),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_H{}_W{}_C{}_nb{}_hs{}_{}_k{}".format(*c[:9]))
+def test_hidden_parity(case):
+    B, H, W, C, nb, hs, dtype, lam, keep, wstd = case
+    wl = synth.Workload("hidden", B, H, W, C, nb, dtype, lam, keep, weight_std=wstd, hidden=hs)
+    say(f"[hidden] B={B} {H}x{W}x{C} nb={nb} bs={C // nb} hidden={hs} {dtype} keep={keep}")
+    x_st, w_st = synth.make_x(wl, seed=3), synth.make_weights(wl, seed=3)
+    w = dev_weights(w_st, dtype)
+    x = to_dev(x_st, dtype)
+    out = afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, lam, keep)
+    torch.cuda.synchronize()
+    ref = oracle_run(x_st, w_st, wl)
+    got = to_f64(out)
+    e_out = max_rel(got, ref)
+    xs = synth.widen(x_st, dtype)
+    msg = f"  out {e_out:.2e}"
+    if dtype == "fp32":
+        e_delta = max_rel(got - xs, ref - xs)
+        msg += f"  delta {e_delta:.2e}"
+        assert e_delta <= 1e-4
+    say(msg)
+    assert e_out <= (1e-4 if dtype == "fp32" else 2e-2)
+
+
+def test_hidden_equal_to_block_size_is_the_default_filter():
+    """hidden == bs through afno_filter_forward_hidden runs the same kernels as
+    afno_filter_forward: bitwise equal outputs."""
+    wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"]
+    x = to_dev(synth.make_x(wl), "bf16")
+    w = dev_weights(synth.make_weights(wl), "bf16")
+    a = afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep)
+    b = torch.empty_like(x)
+    rc = afno.afno_filter_forward_hidden(x.data_ptr(), w["w1"].data_ptr(), w["b1"].data_ptr(),
+                                         w["w2"].data_ptr(), w["b2"].data_ptr(), wl.B, wl.H, wl.W,
+                                         wl.C, wl.num_blocks, wl.C // wl.num_blocks, wl.lam,
+                                         wl.keep, afno.AFNO_DTYPE_BF16, b.data_ptr(),
+                                         torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert rc == afno.AFNO_OK
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
