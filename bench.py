@@ -15,12 +15,13 @@ one event between calls), per-kernel HIP-event times on the launch stream over a
 the roofline of the dominant kernel (algorithmic bytes or FLOPs per launch divided by
 its mean launch time), measured HBM traffic from stored rocprofv3 counters when they
 belong to the current kernel sources, the backward pass on the same workload (dx and the
-parameter gradients for an upstream gradient), the 100-member ensemble workload, the other
+parameter gradients for an upstream gradient), one AFNO block on the same workload (LayerNorm,
+filter, LayerNorm, channel MLP C -> 4C -> C), the 100-member ensemble workload, the other
 workloads' throughput, and the float64 CPU oracle timed on a bounded sample on the host
 cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-backward] [--no-ensemble]
-                    [--no-cpu-baseline] [--no-others]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-backward] [--no-block]
+                    [--no-ensemble] [--no-cpu-baseline] [--no-others]
 """
 from __future__ import annotations
 
@@ -190,6 +191,50 @@ def time_backward(wl, steps: int, warmup: int, seed: int = 0):
             "io_GB_s": round(io_bytes / (ms * 1e-3) / 1e9, 1)}
 
 
+def time_block(wl, steps: int, warmup: int, seed: int = 0):
+    """Mean time of one AFNO block (LayerNorm, filter, LayerNorm, channel MLP C -> 4C -> C,
+    residuals) with inputs resident in HBM; one event pair around all timed calls."""
+    import numpy as np
+    import torch
+
+    import paper_2208_05419_amd as afno
+    from paper_2208_05419_amd import synth
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    x = dev(synth.make_x(wl, seed=seed))
+    p = {k: dev(v) for k, v in synth.make_block_params(wl, seed=seed).items()}
+    out = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        afno.block_forward(x, p, wl.num_blocks, wl.lam, wl.keep, out=out, stream=stream)
+
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < PREWARM_S:
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / steps
+    M = wl.B * wl.H * wl.W
+    mlp_flops = 16 * M * wl.C * wl.C   # two GEMMs M x C x 4C, 2 FLOP per MAC
+    del x, p, out
+    torch.cuda.empty_cache()
+    return {"workload": wl.name, "samples_per_s": round(wl.B / (ms * 1e-3), 2),
+            "ms_per_step": round(ms, 5), "mlp_flops": mlp_flops}
+
+
 def roofline(wl, kern_ms: dict, es: int):
     work = algorithmic_work(wl, es)
     if kern_ms.get("prep", 0.0) < 5e-4:
@@ -282,6 +327,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-others", action="store_true", help="skip the other workloads' timings")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass timing")
+    ap.add_argument("--no-block", action="store_true", help="skip the AFNO-block timing")
+    ap.add_argument("--block-only", action="store_true",
+                    help="time only the AFNO block (one JSON object; for kernel traces)")
     ap.add_argument("--backward-only", action="store_true",
                     help="time only the backward pass (one JSON object; for kernel traces)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -308,6 +356,9 @@ def main():
     if args.backward_only:
         print(json.dumps({"backward": time_backward(wl, args.steps, args.warmup)}), flush=True)
         return
+    if args.block_only:
+        print(json.dumps({"block": time_block(wl, args.steps, args.warmup)}), flush=True)
+        return
     ms, kern_ms, calls, dist = time_workload(wl, args.steps, args.warmup)
     roof, per_kernel = roofline(wl, kern_ms, es)
     value = wl.B / (ms * 1e-3)
@@ -333,6 +384,8 @@ def main():
     }
     if not args.no_backward:
         line["backward"] = time_backward(wl, max(args.steps // 2, 10), max(args.warmup // 2, 3))
+    if not args.no_block:
+        line["block"] = time_block(wl, max(args.steps // 2, 10), max(args.warmup // 2, 3))
     if not args.no_ensemble:
         ens = synth.WORKLOADS["afno90x180_c768_nb8_bf16_ens100_keep0.5"]
         e_ms, e_kern, _, e_dist = time_workload(ens, max(args.steps // 5, 5), max(args.warmup // 5, 3))

@@ -101,6 +101,35 @@ int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, co
                                float keep_fraction, int dtype, void* out, hipStream_t stream);
 
 /*
+ * afno_block_forward -- one AFNO transformer block around the filter: the paper's layer
+ * mixes tokens with the spectral filter and channels with a single-hidden-layer MLP of four
+ * times the embedding width shared by all tokens ("Model Innovations"; "Implementation
+ * Details" (c)).  With per-token LayerNorms (the paper states none; the AFNO layer's pre-norm
+ * arrangement is taken) and the exact GELU:
+ *   t = LN1(x);  v = x + filter(t)  (the filter includes its own residual: filter(t) = t + y);
+ *   w = LN2(v);  out = v + GELU(w wa + ba) wb + bb
+ *   LN(z) = (z - mean) / sqrt(var + 1e-6) * gamma + beta over the C channels of a token,
+ *   biased variance.
+ *   x, out       [B][H][W][C] bf16; tokens are the rows of x viewed as [B*H*W][C]
+ *   ln1_g, ln1_b, ln2_g, ln2_b  [C] bf16, 16-byte aligned
+ *   w1, b1, w2, b2              the filter's weights, as afno_filter_forward
+ *   wa [C][4C], ba [4C], wb [4C][C], bb [C]   bf16, input-major (z wa)
+ * dtype must be AFNO_DTYPE_BF16 (fp32: AFNO_ERR_UNSUPPORTED); C a multiple of 128 and
+ * <= 2048; the filter's limits as afno_filter_forward.  out must not overlap any input
+ * (AFNO_ERR_ALIAS).  The library allocates one stream-ordered workspace (four token grids,
+ * the B*H*W x 4C hidden layer in bf16, the transposed MLP weights and the filter's spectrum)
+ * and frees it stream-ordered.  Intermediates (t, the filter output, v, w, the hidden layer)
+ * are rounded to bf16; products accumulate in fp32.  Other arguments, ownership, errors and
+ * asynchrony as afno_filter_forward.
+ */
+int afno_block_forward(const void* x, const void* ln1_g, const void* ln1_b, const void* w1,
+                       const void* b1, const void* w2, const void* b2, const void* ln2_g,
+                       const void* ln2_b, const void* wa, const void* ba, const void* wb,
+                       const void* bb, int64_t B, int64_t H, int64_t W, int64_t C,
+                       int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                       void* out, hipStream_t stream);
+
+/*
  * afno_filter_stage -- diagnostic entry point: runs the filter's kernels up to a stage
  * and writes that stage's result in float32, for per-stage parity checks.
  *   stage AFNO_STAGE_SPECTRUM  dst [B][H][Wm][C][2] float32: the forward spectrum X

@@ -27,7 +27,7 @@ AFNO_PATH_AUTO = 0
 AFNO_PATH_GENERIC = 1
 AFNO_PATH_VALU_DFT = 2
 
-EXPORTED = ("afno_filter_forward", "afno_filter_forward_hidden", "afno_filter_stage", "afno_filter_backward", "afno_profile_begin",
+EXPORTED = ("afno_filter_forward", "afno_filter_forward_hidden", "afno_block_forward", "afno_filter_stage", "afno_filter_backward", "afno_profile_begin",
             "afno_profile_end", "afno_set_kernel_path", "afno_last_error", "afno_version")
 KERNELS = ("prep", "row_r2c", "column", "row_c2r")
 
@@ -66,6 +66,9 @@ def load_library():
     lib.afno_filter_forward_hidden.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                                f32, f32, ctypes.c_int, vp, vp]
     lib.afno_filter_forward_hidden.restype = ctypes.c_int
+    lib.afno_block_forward.argtypes = [vp] * 13 + [i64, i64, i64, i64, i64, f32, f32,
+                                                   ctypes.c_int, vp, vp]
+    lib.afno_block_forward.restype = ctypes.c_int
     lib.afno_filter_stage.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
                                       ctypes.c_int, ctypes.c_int, vp, vp]
     lib.afno_filter_stage.restype = ctypes.c_int
@@ -209,6 +212,31 @@ def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction
         rc = afno_filter_forward_hidden(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W,
                                         C, num_blocks, hs, lam, keep_fraction, _dtype_code(x),
                                         _ptr(out), _stream(stream))
+    _check(rc)
+    return out
+
+
+def afno_block_forward(x, ln1_g, ln1_b, w1, b1, w2, b2, ln2_g, ln2_b, wa, ba, wb, bb, B, H, W, C,
+                       num_blocks, lam, keep_fraction, dtype, out, stream) -> int:
+    """Raw call: pointers as ints (or None), returns the C return code."""
+    return load_library().afno_block_forward(x, ln1_g, ln1_b, w1, b1, w2, b2, ln2_g, ln2_b, wa,
+                                             ba, wb, bb, B, H, W, C, num_blocks, lam,
+                                             keep_fraction, dtype, out, stream)
+
+
+BLOCK_PARAMS = ("ln1_g", "ln1_b", "w1", "b1", "w2", "b2", "ln2_g", "ln2_b", "wa", "ba", "wb", "bb")
+
+
+def block_forward(x, p: dict, num_blocks: int, lam: float, keep_fraction: float = 1.0, out=None,
+                  stream=None):
+    """One AFNO block on x [B,H,W,C] bfloat16: p holds the BLOCK_PARAMS tensors (bfloat16, on
+    the GPU).  Enqueued on ``stream`` (default: torch's current stream)."""
+    import torch
+    B, H, W, C = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    rc = afno_block_forward(_ptr(x), *(_ptr(p[k]) for k in BLOCK_PARAMS), B, H, W, C, num_blocks,
+                            lam, keep_fraction, _dtype_code(x), _ptr(out), _stream(stream))
     _check(rc)
     return out
 

@@ -295,6 +295,68 @@ int run_backward(const Args& a, const void* gout, float* dw1, float* db1, float*
   return AFNO_OK;
 }
 
+// One AFNO block: validation, the filter's plan for the block's shape, one workspace.
+int run_block(const Args& a, const void* ln1_g, const void* ln1_b, const void* ln2_g,
+              const void* ln2_b, const void* wa, const void* ba, const void* wb, const void* bb,
+              hipStream_t stream) {
+  if (a.dtype != AFNO_DTYPE_BF16 && a.dtype != AFNO_DTYPE_FP32)
+    return fail(AFNO_ERR_INVALID_ARG, "dtype must be AFNO_DTYPE_FP32 (0) or AFNO_DTYPE_BF16 (1)");
+  afno::Plan pl;
+  int rc = make_plan(a, pl);
+  if (rc != AFNO_OK) return rc;
+  if (a.dtype != AFNO_DTYPE_BF16)
+    return fail(AFNO_ERR_UNSUPPORTED, "the AFNO block runs in bf16 storage only");
+  if (a.C % 128 != 0 || a.C > 2048)
+    return fail(AFNO_ERR_UNSUPPORTED, "the AFNO block needs C a multiple of 128 and <= 2048");
+  if (a.B == 0) return AFNO_OK;
+  const void* vecs[] = {ln1_g, ln1_b, ln2_g, ln2_b};
+  for (const void* p : vecs)
+    if (!p) return fail(AFNO_ERR_INVALID_ARG, "null pointer argument");
+  if (!wa || !ba || !wb || !bb) return fail(AFNO_ERR_INVALID_ARG, "null pointer argument");
+  for (const void* p : vecs)
+    if (!aligned(p, 16)) return fail(AFNO_ERR_UNSUPPORTED, "LayerNorm weights must be 16-byte aligned");
+  if (!aligned(wa, 2) || !aligned(ba, 2) || !aligned(wb, 2) || !aligned(bb, 2))
+    return fail(AFNO_ERR_UNSUPPORTED, "MLP weights must be 2-byte aligned");
+  const size_t xb = (size_t)a.B * a.H * a.W * a.C * 2;
+  const size_t cb = (size_t)a.C * 2, mb = (size_t)a.C * 4 * a.C * 2;
+  struct R { const void* p; size_t n; };
+  const R ins[] = {{ln1_g, cb}, {ln1_b, cb}, {ln2_g, cb}, {ln2_b, cb}, {wa, mb}, {ba, 4 * cb},
+                   {wb, mb}, {bb, cb}};
+  for (const R& i : ins)
+    if (overlaps(a.out, xb, i.p, i.n)) return fail(AFNO_ERR_ALIAS, "out overlaps an input");
+
+  std::call_once(g_attr_once, [] {
+    (void)afno::set_kernel_attributes();
+    (void)hipGetLastError();
+  });
+  auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t M = (size_t)a.B * a.H * a.W;
+  afno::BlockPtrs bp{a.x, ln1_g, ln1_b, a.w1, a.b1, a.w2, a.b2, ln2_g, ln2_b, wa, ba, wb, bb,
+                     a.out, nullptr, 0, 0, 0, 0, 0, 0, 0, 0};
+  bp.t_off = 0;
+  bp.u_off = up(xb);
+  bp.v_off = bp.u_off + up(xb);
+  bp.w_off = bp.v_off + up(xb);
+  bp.h_off = bp.w_off + up(xb);
+  bp.wat_off = bp.h_off + up(M * 4 * a.C * 2);
+  bp.wbt_off = bp.wat_off + up(mb);
+  bp.s_off = bp.wbt_off + up(mb);
+  const size_t bytes = bp.s_off + pl.ws_bytes;
+  void* ws = nullptr;
+  hipError_t e = hipMallocAsync(&ws, bytes, stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") + std::to_string(bytes) +
+                                  " bytes: " + hipGetErrorString(e));
+  }
+  bp.ws = static_cast<char*>(ws);
+  e = afno::launch_block(pl, bp, stream);
+  hipError_t ef = hipFreeAsync(ws, stream);
+  if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
+  if (ef != hipSuccess) return fail(AFNO_ERR_HIP, std::string("workspace free: ") + hipGetErrorString(ef));
+  return AFNO_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -316,6 +378,17 @@ int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, co
   if (hidden <= 0) return fail(AFNO_ERR_INVALID_ARG, "hidden must be > 0");
   Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0, hidden};
   return run(a, afno::kStageFull, nullptr, stream);
+}
+
+int afno_block_forward(const void* x, const void* ln1_g, const void* ln1_b, const void* w1,
+                       const void* b1, const void* w2, const void* b2, const void* ln2_g,
+                       const void* ln2_b, const void* wa, const void* ba, const void* wb,
+                       const void* bb, int64_t B, int64_t H, int64_t W, int64_t C,
+                       int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                       void* out, hipStream_t stream) {
+  g_last_error.clear();
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0, 0};
+  return run_block(a, ln1_g, ln1_b, ln2_g, ln2_b, wa, ba, wb, bb, stream);
 }
 
 int afno_filter_stage(const void* x, const void* w1, const void* b1, const void* w2,

@@ -70,6 +70,14 @@ struct BwdPtrs {
   void* ws;
 };
 
+// pointers of one AFNO-block call (all bf16) and its workspace offsets
+struct BlockPtrs {
+  const void *x, *ln1_g, *ln1_b, *w1, *b1, *w2, *b2, *ln2_g, *ln2_b, *wa, *ba, *wb, *bb;
+  void* out;
+  char* ws;
+  size_t t_off, u_off, v_off, w_off, h_off, wat_off, wbt_off, s_off;
+};
+
 hipError_t set_kernel_attributes();
 // 0: specialised kernels where available, 1: generic only, 2: as 0 without the
 // MFMA-transform column kernel
@@ -90,6 +98,9 @@ size_t bwd_acc_floats(const Plan& pl);  // fp32 sums of the weight and bias grad
 int wgrad_slab_chunks(const Plan& pl, int* kchunk);
 hipError_t launch_backward(const Plan& pl, const BwdPtrs& a, hipStream_t st);
 hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st);
+// one AFNO block (LayerNorm, filter, LayerNorm, channel MLP, residuals); pl: the filter's
+// plan for the block's shape
+hipError_t launch_block(const Plan& pl, const BlockPtrs& a, hipStream_t st);
 hipError_t launch_filter(const Plan& pl, const void* x, const void* w1, const void* b1,
                          const void* w2, const void* b2, void* S, void* out, float* dst,
                          int stage, hipStream_t st, hipEvent_t* ev);

@@ -20,6 +20,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "afno_internal.h"
 #include "kernels_fast.h"
@@ -27,6 +28,7 @@
 #include "kernels_mfma.h"
 #include "kernels_backward.h"
 #include "kernels_backward_mfma.h"
+#include "kernels_block.h"
 
 namespace afno {
 
@@ -444,6 +446,56 @@ hipError_t launch_zero_grads(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ AFNO block
+
+hipError_t launch_block(const Plan& pl, const BlockPtrs& a, hipStream_t st) {
+  const int64_t M = pl.B * pl.H * pl.W;
+  const int C = (int)pl.C, N1 = 4 * C;
+  char* ws = a.ws;
+  bf16* t = reinterpret_cast<bf16*>(ws + a.t_off);
+  bf16* u = reinterpret_cast<bf16*>(ws + a.u_off);
+  bf16* v = reinterpret_cast<bf16*>(ws + a.v_off);
+  bf16* w = reinterpret_cast<bf16*>(ws + a.w_off);
+  bf16* h = reinterpret_cast<bf16*>(ws + a.h_off);
+  bf16* wat = reinterpret_cast<bf16*>(ws + a.wat_off);
+  bf16* wbt = reinterpret_cast<bf16*>(ws + a.wbt_off);
+  const bf16* x = static_cast<const bf16*>(a.x);
+  // the MLP weights in the GEMM's [N][K] form
+  hipLaunchKernelGGL(transpose_bf16, dim3((unsigned)((N1 + 31) / 32), (unsigned)((C + 31) / 32)),
+                     dim3(256), 0, st, static_cast<const bf16*>(a.wa), wat, C, N1);
+  hipLaunchKernelGGL(transpose_bf16, dim3((unsigned)((C + 31) / 32), (unsigned)((N1 + 31) / 32)),
+                     dim3(256), 0, st, static_cast<const bf16*>(a.wb), wbt, N1, C);
+  const unsigned lng = (unsigned)((M + 3) / 4);
+  hipLaunchKernelGGL(layer_norm_kernel, dim3(lng), dim3(256), 0, st, x,
+                     static_cast<const bf16*>(a.ln1_g), static_cast<const bf16*>(a.ln1_b), t, M, C);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_filter(pl, t, a.w1, a.b1, a.w2, a.b2, ws + a.s_off, u, nullptr, kStageFull, st,
+                    nullptr);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(add_layer_norm_kernel, dim3(lng), dim3(256), 0, st, u, x,
+                     static_cast<const bf16*>(a.ln2_g), static_cast<const bf16*>(a.ln2_b), v, w, M, C);
+  // row tiles of 256, padded to whole XCD rounds; column tiles of 256 where N allows
+  const int64_t mbp = ((M + 255) / 256 + 7) / 8 * 8;
+  auto gemm = [&](auto epi, const bf16* Am, const bf16* Bm, const bf16* bias, const bf16* Rm,
+                  bf16* Dm, int N, int K) {
+    constexpr int E = decltype(epi)::value;
+    if (N % 256 == 0)
+      hipLaunchKernelGGL((gemm_bf16<E, 256>), dim3((unsigned)(mbp * (N / 256))),
+                         dim3(GemmGeo<256>::NT), GemmGeo<256>::kBytes, st, Am, Bm, bias, Rm, Dm,
+                         (int)M, N, K);
+    else
+      hipLaunchKernelGGL((gemm_bf16<E, 128>), dim3((unsigned)(mbp * (N / 128))),
+                         dim3(GemmGeo<128>::NT), GemmGeo<128>::kBytes, st, Am, Bm, bias, Rm, Dm,
+                         (int)M, N, K);
+  };
+  gemm(std::integral_constant<int, kEpiGelu>(), w, wat, static_cast<const bf16*>(a.ba), nullptr, h,
+       N1, C);
+  gemm(std::integral_constant<int, kEpiResidual>(), h, wbt, static_cast<const bf16*>(a.bb), v,
+       static_cast<bf16*>(a.out), C, N1);
+  return hipGetLastError();
+}
+
 hipError_t set_kernel_attributes() {
   const int lds_max = kLdsBytes;
   hipError_t e, first = hipSuccess;
@@ -459,6 +511,10 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(column_kernel<bf16>)
   AFNO_ATTR(column_bwd_kernel<float>)
   AFNO_ATTR(column_bwd_kernel<bf16>)
+  AFNO_ATTR((gemm_bf16<kEpiGelu, 128>))
+  AFNO_ATTR((gemm_bf16<kEpiGelu, 256>))
+  AFNO_ATTR((gemm_bf16<kEpiResidual, 128>))
+  AFNO_ATTR((gemm_bf16<kEpiResidual, 256>))
   AFNO_ATTR(wgrad_slab<64>)
   AFNO_ATTR(wgrad_slab<128>)
   AFNO_ATTR(wgrad_slab<192>)

@@ -1,0 +1,305 @@
+// kernels_block.h -- the rest of one AFNO transformer block around the spectral filter:
+// per-token LayerNorm, the channel-mixing MLP (C -> 4C -> C, shared by all tokens, "Model
+// Innovations" and "Implementation Details" (c)) as two bf16 matrix-core GEMMs with fused
+// epilogues, and the residual adds.  Tokens are the rows of x [B H W][C] (row-major).
+//
+//   t   = LN1(x)                         layer_norm_kernel
+//   u   = filter(t)  (= t + y(t))         the filter's kernels
+//   v   = u + x,  w = LN2(v)              add_layer_norm_kernel
+//   h   = GELU(w Wa + ba)                 gemm_bf16<kEpiGelu>
+//   out = v + h Wb + bb                   gemm_bf16<kEpiResidual>
+#pragma once
+#include "kernel_common.h"
+#include "kernels_mfma.h"
+
+namespace afno {
+
+constexpr int kLnMaxPerLane = 32;  // values a lane holds: C <= 64 * 32
+constexpr float kLnEps = 1e-6f;
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// LayerNorm of one token's C channels held as vals[0 .. n) by this lane (channels
+// 8 (lane + 64 i) .. + 7 for chunk i), two passes over registers; writes bf16.
+template <int NCH>
+__device__ __forceinline__ void ln_token(float (&vals)[NCH][8], int nchunk, int C, int lane,
+                                         const bf16* __restrict__ gamma,
+                                         const bf16* __restrict__ beta, bf16* __restrict__ y) {
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NCH; ++i)
+    if (lane + 64 * i < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += vals[i][e];
+    }
+  const float mean = wave_sum(s) / (float)C;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NCH; ++i)
+    if (lane + 64 * i < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = vals[i][e] - mean;
+        q += d * d;
+      }
+    }
+  const float rstd = rsqrtf(wave_sum(q) / (float)C + kLnEps);
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nchunk) {
+      const uint4 gw = *reinterpret_cast<const uint4*>(gamma + 8 * ch);
+      const uint4 bw = *reinterpret_cast<const uint4*>(beta + 8 * ch);
+      const uint32_t* gu = reinterpret_cast<const uint32_t*>(&gw);
+      const uint32_t* bu = reinterpret_cast<const uint32_t*>(&bw);
+      uint32_t o[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const float g0 = __uint_as_float(gu[p] << 16), g1 = __uint_as_float(gu[p] & 0xffff0000u);
+        const float b0 = __uint_as_float(bu[p] << 16), b1 = __uint_as_float(bu[p] & 0xffff0000u);
+        o[p] = cvt_pk((vals[i][2 * p] - mean) * rstd * g0 + b0,
+                      (vals[i][2 * p + 1] - mean) * rstd * g1 + b1);
+      }
+      *reinterpret_cast<uint4*>(y + 8 * ch) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+__device__ __forceinline__ void unpack8(uint4 w, float (&v)[8]) {
+  const uint32_t* u = reinterpret_cast<const uint32_t*>(&w);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    v[2 * p] = __uint_as_float(u[p] << 16);
+    v[2 * p + 1] = __uint_as_float(u[p] & 0xffff0000u);
+  }
+}
+
+// y = LN(x) per token; one wave per token, 4 tokens per 256-thread workgroup.  C a multiple
+// of 8, at most 64 * kLnMaxPerLane.
+__global__ void __launch_bounds__(256) layer_norm_kernel(const bf16* __restrict__ x,
+                                                         const bf16* __restrict__ gamma,
+                                                         const bf16* __restrict__ beta,
+                                                         bf16* __restrict__ y, int64_t M, int C) {
+  constexpr int NCH = kLnMaxPerLane / 8;
+  const int lane = threadIdx.x & 63;
+  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= M) return;
+  const int nchunk = C / 8;
+  const bf16* xr = x + tok * C;
+  float vals[NCH][8];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nchunk) unpack8(*reinterpret_cast<const uint4*>(xr + 8 * ch), vals[i]);
+  }
+  ln_token<NCH>(vals, nchunk, C, lane, gamma, beta, y + tok * C);
+}
+
+// v = u + x (rounded to bf16 and stored), w = LN(v) of the stored v; as layer_norm_kernel.
+__global__ void __launch_bounds__(256) add_layer_norm_kernel(const bf16* __restrict__ u,
+                                                             const bf16* __restrict__ x,
+                                                             const bf16* __restrict__ gamma,
+                                                             const bf16* __restrict__ beta,
+                                                             bf16* __restrict__ v,
+                                                             bf16* __restrict__ w, int64_t M, int C) {
+  constexpr int NCH = kLnMaxPerLane / 8;
+  const int lane = threadIdx.x & 63;
+  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= M) return;
+  const int nchunk = C / 8;
+  float vals[NCH][8];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nchunk) {
+      float a[8], b[8];
+      unpack8(*reinterpret_cast<const uint4*>(u + tok * C + 8 * ch), a);
+      unpack8(*reinterpret_cast<const uint4*>(x + tok * C + 8 * ch), b);
+      uint32_t o[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) o[p] = cvt_pk(a[2 * p] + b[2 * p], a[2 * p + 1] + b[2 * p + 1]);
+      const uint4 ow = make_uint4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<uint4*>(v + tok * C + 8 * ch) = ow;
+      unpack8(ow, vals[i]);  // LN of the stored (rounded) v
+    }
+  }
+  ln_token<NCH>(vals, nchunk, C, lane, gamma, beta, w + tok * C);
+}
+
+// dst[c][r] = src[r][c] for a rows x cols bf16 matrix (weights to the GEMM's [N][K] form)
+__global__ void __launch_bounds__(256) transpose_bf16(const bf16* __restrict__ src,
+                                                      bf16* __restrict__ dst, int rows, int cols) {
+  __shared__ uint16_t t[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const uint16_t* s = reinterpret_cast<const uint16_t*>(src);
+  uint16_t* d = reinterpret_cast<uint16_t*>(dst);
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int i = ty; i < 32; i += 8) {
+    const int r = r0 + i, c = c0 + tx;
+    t[i][tx] = (r < rows && c < cols) ? s[(int64_t)r * cols + c] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) d[(int64_t)c * rows + r] = t[tx][i];
+  }
+}
+
+enum { kEpiGelu = 0, kEpiResidual = 1 };
+
+// GEMM geometry: workgroup tile 256 x BN (rows x columns of D, BN = 128 or 256), k-stage 32;
+// 4 x (BN / 64) waves, each 64 x 64 (4 x 4 MFMA tiles of 16 x 16).  LDS: two stages of the A
+// (256 x 32) and B (BN x 32) slabs, rows padded to 40 elements; the epilogue reuses it for
+// 64 rows of fp32 at a time.  (Measured on the block's 64800 x 3072 x 768 and 64800 x 768 x
+// 3072 products: 256 x 256 with 16 waves ahead of 256 x 128 with 8, 128 x 128 with 4, and of
+// 64-deep stages, whose one workgroup per CU leaves the next stage's load latency exposed.)
+template <int BN>
+struct GemmGeo {
+  static constexpr int BM = 256, BK = 32, LDK = BK + 8;
+  static constexpr int NWN = BN / 64, NT = 64 * 4 * NWN;    // threads
+  static constexpr int ASLAB = BM * LDK, BSLAB = BN * LDK;
+  static constexpr int STAGE = ASLAB + BSLAB;               // elements
+  static constexpr int LDC = BN + 4;                         // epilogue stride, floats
+  static constexpr int kLA = BM * (BK / 8) / NT, kLB = BN * (BK / 8) / NT;  // words per thread
+  static constexpr int kBytes = 2 * STAGE * 2 > 64 * LDC * 4 ? 2 * STAGE * 2 : 64 * LDC * 4;
+  static_assert(BM * (BK / 8) % NT == 0 && BN * (BK / 8) % NT == 0, "whole words per thread");
+};
+
+// D[M][N] = epi(A[M][K] Bt[N][K]^T + bias[N]) in bf16, fp32 accumulation on the matrix cores.
+// The next k-stage's global loads are in flight during the current stage's products.
+// Epilogue: + bias staged through LDS in fp32 (64 rows at a time), then, on the way out to
+// row-contiguous stores, GELU (kEpiGelu) or + R[M][N] (kEpiResidual).  Rows of A past M are read clamped and never
+// stored.  Tiles go XCD-aware: workgroup g runs on XCD g % 8 and the workgroups of one XCD
+// take all column tiles of a row tile in turn, so that row tile's A stays in that XCD's L2.
+// N a multiple of BN, K a multiple of 32; grid 8 ceil(MB / 8) (N / BN) with MB = ceil(M / 256);
+// GemmGeo<BN>::NT threads; dynamic LDS GemmGeo<BN>::kBytes.
+template <int EPI, int BN>
+__global__ void __launch_bounds__(GemmGeo<BN>::NT) gemm_bf16(const bf16* __restrict__ A,
+                                                             const bf16* __restrict__ Bt,
+                                                             const bf16* __restrict__ bias,
+                                                             const bf16* __restrict__ R,
+                                                             bf16* __restrict__ D, int M, int N,
+                                                             int K) {
+  typedef GemmGeo<BN> G;
+  extern __shared__ uint4 gemm_smem[];
+  bf16* S = reinterpret_cast<bf16*>(gemm_smem);           // [2][STAGE]: A slab, then B slab
+  float* sC = reinterpret_cast<float*>(gemm_smem);        // [64][LDC] in the epilogue
+
+  const int nbn = N / BN;
+  const int g = blockIdx.x, xcd = g & 7, i = g >> 3;
+  const int mb = (i / nbn) * 8 + xcd, nbk = i - (i / nbn) * nbn;
+  const int m0 = mb * G::BM, n0 = nbk * BN;
+  if (m0 >= M) return;  // padding workgroups: the whole group leaves before any barrier
+
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, gq = lane >> 4;
+  const int wave = tid >> 6, wm = wave / G::NWN, wn = wave % G::NWN;
+  // global -> LDS: thread tid moves k-word tid % 4 of rows tid / 4 + RS j (A: kLA rows, B: kLB)
+  constexpr int RS = G::NT / 4;
+  const int r4 = tid >> 2, kc = 8 * (tid & 3);
+  const bf16* srcB = Bt + (int64_t)(n0 + r4) * K + kc;
+  int64_t aoff[G::kLA];
+#pragma unroll
+  for (int j = 0; j < G::kLA; ++j) aoff[j] = (int64_t)min(m0 + r4 + RS * j, M - 1) * K + kc;
+  const int dA = r4 * G::LDK + kc, dB = G::ASLAB + r4 * G::LDK + kc;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int stages = K / G::BK;
+  {
+    uint4 ra[G::kLA], rb[G::kLB];
+#pragma unroll
+    for (int j = 0; j < G::kLA; ++j) ra[j] = *reinterpret_cast<const uint4*>(A + aoff[j]);
+#pragma unroll
+    for (int j = 0; j < G::kLB; ++j)
+      rb[j] = *reinterpret_cast<const uint4*>(srcB + (int64_t)RS * j * K);
+#pragma unroll
+    for (int j = 0; j < G::kLA; ++j) *reinterpret_cast<uint4*>(S + dA + RS * j * G::LDK) = ra[j];
+#pragma unroll
+    for (int j = 0; j < G::kLB; ++j) *reinterpret_cast<uint4*>(S + dB + RS * j * G::LDK) = rb[j];
+  }
+  __syncthreads();
+  for (int s = 0; s < stages; ++s) {
+    const int buf = s & 1;
+    // the next stage's words (the last stage reloads its own: loads and stores unconditional)
+    const int kn = (s + 1 < stages ? s + 1 : s) * G::BK;
+    uint4 na[G::kLA], nb_[G::kLB];
+#pragma unroll
+    for (int j = 0; j < G::kLA; ++j) na[j] = *reinterpret_cast<const uint4*>(A + aoff[j] + kn);
+#pragma unroll
+    for (int j = 0; j < G::kLB; ++j)
+      nb_[j] = *reinterpret_cast<const uint4*>(srcB + (int64_t)RS * j * K + kn);
+    const bf16* cA = S + buf * G::STAGE + (64 * wm + l16) * G::LDK + 8 * gq;
+    const bf16* cB = S + buf * G::STAGE + G::ASLAB + (64 * wn + l16) * G::LDK + 8 * gq;
+    uint4 fa[4], fb[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) fa[a] = *reinterpret_cast<const uint4*>(cA + 16 * a * G::LDK);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) fb[b] = *reinterpret_cast<const uint4*>(cB + 16 * b * G::LDK);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = mma_bf16(fa[a], fb[b], acc[a][b]);
+    bf16* nS = S + (buf ^ 1) * G::STAGE;
+#pragma unroll
+    for (int j = 0; j < G::kLA; ++j) *reinterpret_cast<uint4*>(nS + dA + RS * j * G::LDK) = na[j];
+#pragma unroll
+    for (int j = 0; j < G::kLB; ++j) *reinterpret_cast<uint4*>(nS + dB + RS * j * G::LDK) = nb_[j];
+    __syncthreads();
+  }
+
+  // ---- epilogue, one wave row (64 rows) at a time
+  float bv[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) bv[b] = (float)bias[n0 + 64 * wn + 16 * b + l16];
+  constexpr int C4 = BN / 4;              // groups of 4 columns per row
+  constexpr int PER = 64 * C4 / G::NT;    // groups per thread
+#pragma unroll 1
+  for (int part = 0; part < 4; ++part) {
+    if (wm == part) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            sC[(16 * a + 4 * gq + q) * G::LDC + 64 * wn + 16 * b + l16] = acc[a][b][q] + bv[b];
+          }
+    }
+    __syncthreads();
+#pragma unroll 1
+    for (int j = 0; j < PER; ++j) {
+      const int c = tid + G::NT * j;
+      const int r = c / C4, c4 = 4 * (c - (c / C4) * C4);
+      const int row = m0 + 64 * part + r;
+      if (row < M) {
+        const float4 z = *reinterpret_cast<const float4*>(sC + r * G::LDC + c4);
+        float o0 = z.x, o1 = z.y, o2 = z.z, o3 = z.w;
+        if constexpr (EPI == kEpiGelu) {  // GELU(z) = z Phi(z) = 0.5 z (1 + erf(z / sqrt 2))
+          o0 = 0.5f * o0 * (1.f + erff(o0 * 0.70710678118654752f));
+          o1 = 0.5f * o1 * (1.f + erff(o1 * 0.70710678118654752f));
+          o2 = 0.5f * o2 * (1.f + erff(o2 * 0.70710678118654752f));
+          o3 = 0.5f * o3 * (1.f + erff(o3 * 0.70710678118654752f));
+        }
+        const int64_t off = (int64_t)row * N + n0 + c4;
+        if constexpr (EPI == kEpiResidual) {
+          const uint2 rw = *reinterpret_cast<const uint2*>(R + off);
+          o0 += __uint_as_float(rw.x << 16);
+          o1 += __uint_as_float(rw.x & 0xffff0000u);
+          o2 += __uint_as_float(rw.y << 16);
+          o3 += __uint_as_float(rw.y & 0xffff0000u);
+        }
+        *reinterpret_cast<uint2*>(D + off) = make_uint2(cvt_pk(o0, o1), cvt_pk(o2, o3));
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace afno

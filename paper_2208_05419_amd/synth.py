@@ -146,3 +146,20 @@ def widen(stored: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "fp32":
         return np.asarray(stored, dtype=np.float32).astype(np.float64)
     return bf16_bits_to_f32(stored).astype(np.float64)
+
+
+def make_block_params(wl: Workload, seed: int = 0, mlp_std: float = 0.02) -> dict:
+    """Parameters of one AFNO block around the filter, stored form: LayerNorm gains 1 + 0.1 N,
+    shifts 0.1 N over C; the channel MLP wa [C][4C], ba [4C], wb [4C][C], bb [C] with std
+    mlp_std (biases 0.1 mlp_std); and the filter's weights (make_weights)."""
+    C = wl.C
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 5]))
+    p = dict(make_weights(wl, seed=seed))
+    raw = {
+        "ln1_g": 1.0 + 0.1 * rng.standard_normal(C), "ln1_b": 0.1 * rng.standard_normal(C),
+        "ln2_g": 1.0 + 0.1 * rng.standard_normal(C), "ln2_b": 0.1 * rng.standard_normal(C),
+        "wa": mlp_std * rng.standard_normal((C, 4 * C)), "ba": 0.1 * mlp_std * rng.standard_normal(4 * C),
+        "wb": mlp_std * rng.standard_normal((4 * C, C)), "bb": 0.1 * mlp_std * rng.standard_normal(C),
+    }
+    p.update({k: quantize(v, wl.dtype) for k, v in raw.items()})
+    return p

@@ -175,3 +175,38 @@ def test_hidden_alias_covers_the_wider_weights():
     # w1 is nb * bs * hidden * 2 * 4 = 4 * 16 * 32 * 8 = 16 KiB: out 12 KiB after w1 overlaps it
     assert call_hidden(out=W1 + 12 * 1024) == afno.AFNO_ERR_ALIAS
     assert call_hidden(out=B1 + 256) == afno.AFNO_ERR_ALIAS   # b1: 4 * 32 * 8 = 1 KiB
+
+
+LN = [0x10000000 * (i + 20) for i in range(8)]  # ln1_g, ln1_b, ln2_g, ln2_b, wa, ba, wb, bb
+
+
+def call_block(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, ln1_g=LN[0], ln1_b=LN[1], ln2_g=LN[2], ln2_b=LN[3],
+             wa=LN[4], ba=LN[5], wb=LN[6], bb=LN[7], B=1, H=16, W=32, C=128, nb=4, lam=0.01,
+             keep=1.0, dtype=afno.AFNO_DTYPE_BF16, out=OUT)
+    a.update(kw)
+    return afno.afno_block_forward(a["x"], a["ln1_g"], a["ln1_b"], a["w1"], a["b1"], a["w2"],
+                                   a["b2"], a["ln2_g"], a["ln2_b"], a["wa"], a["ba"], a["wb"],
+                                   a["bb"], a["B"], a["H"], a["W"], a["C"], a["nb"], a["lam"],
+                                   a["keep"], a["dtype"], a["out"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(ln1_g=None), dict(wb=None), dict(x=None), dict(C=128, nb=3),
+                                dict(dtype=7), dict(lam=float("nan"))])
+def test_block_invalid_arguments(kw):
+    assert call_block(**kw) == afno.AFNO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(dtype=afno.AFNO_DTYPE_FP32), dict(C=64, nb=4),
+                                dict(C=4096, nb=32), dict(ln2_b=LN[3] + 8), dict(H=7)])
+def test_block_unsupported(kw):
+    assert call_block(**kw) == afno.AFNO_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kw", [dict(out=LN[4] + 64), dict(out=X), dict(out=W2 + 16)])
+def test_block_alias(kw):
+    assert call_block(**kw) == afno.AFNO_ERR_ALIAS
+
+
+def test_block_empty_batch_is_ok_without_the_gpu():
+    assert call_block(B=0, x=None, out=None) == afno.AFNO_OK
