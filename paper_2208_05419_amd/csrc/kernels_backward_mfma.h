@@ -25,6 +25,14 @@
 #include "kernels_mfma.h"
 
 namespace afno {
+// An opaque copy of a value: the compiler cannot tie expressions of the copy to expressions
+// of the original, so each phase of the column kernel derives its lane indices afresh instead
+// of keeping seven phases' worth of index arithmetic live (which spilled 35 VGPRs at 96 x 96).
+__device__ __forceinline__ int opq(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 
 template <int HP, int BS>
 struct MfmaBwd {
@@ -110,7 +118,7 @@ __device__ __forceinline__ void bwd_load_planes(bf16* P, const Buf& cb, int H, u
   typedef MfmaCol<HP, BS> G;
   constexpr int XT = BS * (HP / 8);
   constexpr int XR = (XT + G::kThreads - 1) / G::kThreads;
-  const int tid = threadIdx.x;
+  const int tid = opq((int)threadIdx.x);  // not shared with the other column load's offsets
   uint32_t xv[XR][8];
 #pragma unroll
   for (int u = 0; u < XR; ++u) {
@@ -285,7 +293,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_bmfma) + G::kTabBytes);
   uint32_t* M1 = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(R) + G::kRegionBytes);
   uint32_t* M2 = M1 + HP * NW1;  // M1[k][NW1]: v > 0;  M2[entry][NW2]: |o| > lam, kept
-  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x;  // each phase takes its own lane indices (opq)
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int twm = wave / G::TWN, twn = wave % G::TWN;
   const int lwm = wave / G::LWN, lwn = wave % G::LWN;
@@ -312,6 +320,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P1: X^T = DFT(x) -> Y[k][entry]
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
     bwd_dft_acc<HP, BS>(R, dtab_lo, lane, twm, twn, 0, acc);
@@ -331,6 +340,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P2: H^T = relu(W1x^T Y^T + b1) -> H[k][hidden]; bits v > 0
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     bwd_prod_wt<HP, BS>(Buf(wfwd + blk * kBlockWords, (uint32_t)(kBlockWords * 16)), 0, R, lane,
                         twm, twn, acc);
@@ -370,6 +380,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P3: O = H W2x + b2 -> bits |o| > lam on kept rows
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::LMW][G::LNW];
     bwd_prod_tw<HP, BS>(Buf(wfwd + blk * kBlockWords, (uint32_t)(kBlockWords * 16)), kLayerBytes,
                         R, lane, lwm, lwn, acc);
@@ -398,6 +409,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   bwd_load_planes<HP, BS>(R, Buf(Sg + coff, cbytes), H, rsb);
   __syncthreads();
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
     __syncthreads();
@@ -423,6 +435,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P5: dh^T = W2x do^T, dv = dh where v > 0 -> DV[k][hidden]
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     bwd_prod_wt<HP, BS>(Buf(wbwd + blk * kBlockWords, (uint32_t)(kBlockWords * 16)), 0, R, lane,
                         twm, twn, acc);
@@ -447,6 +460,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P6: dX = DV W1x^T -> planes [rho][c][k]
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::LMW][G::LNW];
     bwd_prod_tw<HP, BS>(Buf(wbwd + blk * kBlockWords, (uint32_t)(kBlockWords * 16)), kLayerBytes,
                         R, lane, lwm, lwn, acc);
@@ -466,6 +480,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
 
   // ---- P7: Z^T = IDFT(dX) / c_kw -> Z[h][entry] -> the column of Sg
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 1, acc);
     __syncthreads();
