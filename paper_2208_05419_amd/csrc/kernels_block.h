@@ -151,15 +151,16 @@ __global__ void __launch_bounds__(256) transpose_bf16(const bf16* __restrict__ s
 
 enum { kEpiGelu = 0, kEpiResidual = 1 };
 
-// GEMM geometry: workgroup tile 256 x BN (rows x columns of D, BN = 128 or 256), k-stage 32;
-// 4 x (BN / 64) waves, each 64 x 64 (4 x 4 MFMA tiles of 16 x 16).  LDS: two stages of the A
-// (256 x 32) and B (BN x 32) slabs, rows padded to 40 elements; the epilogue reuses it for
-// 64 rows of fp32 at a time.  (Measured on the block's 64800 x 3072 x 768 and 64800 x 768 x
-// 3072 products: 256 x 256 with 16 waves ahead of 256 x 128 with 8, 128 x 128 with 4, and of
-// 64-deep stages, whose one workgroup per CU leaves the next stage's load latency exposed.)
+// GEMM geometry: workgroup tile 256 x BN (rows x columns of D, BN = 128 or 256), k-stage 64
+// (two MFMA k-steps per barrier); 4 x (BN / 64) waves, each 64 x 64 (4 x 4 MFMA tiles of
+// 16 x 16).  LDS: two stages of the A (256 x 64) and B (BN x 64) slabs, rows padded to 72
+// elements (147 KB at BN = 256: one workgroup per CU); the epilogue reuses it for 64 rows of
+// fp32 at a time.  (Measured on the block's 64800 x 3072 x 768 and 64800 x 768 x 3072
+// products: 256 x 256 with 16 waves ahead of 256 x 128 with 8 and 128 x 128 with 4; 64-deep
+// stages 3-9 % ahead of 32-deep ones at this tile.)
 template <int BN>
 struct GemmGeo {
-  static constexpr int BM = 256, BK = 32, LDK = BK + 8;
+  static constexpr int BM = 256, BK = 64, LDK = BK + 8;
   static constexpr int NWN = BN / 64, NT = 64 * 4 * NWN;    // threads
   static constexpr int ASLAB = BM * LDK, BSLAB = BN * LDK;
   static constexpr int STAGE = ASLAB + BSLAB;               // elements
@@ -175,7 +176,7 @@ struct GemmGeo {
 // row-contiguous stores, GELU (kEpiGelu) or + R[M][N] (kEpiResidual).  Rows of A past M are read clamped and never
 // stored.  Tiles go XCD-aware: workgroup g runs on XCD g % 8 and the workgroups of one XCD
 // take all column tiles of a row tile in turn, so that row tile's A stays in that XCD's L2.
-// N a multiple of BN, K a multiple of 32; grid 8 ceil(MB / 8) (N / BN) with MB = ceil(M / 256);
+// N a multiple of BN, K a multiple of 64; grid 8 ceil(MB / 8) (N / BN) with MB = ceil(M / 256);
 // GemmGeo<BN>::NT threads; dynamic LDS GemmGeo<BN>::kBytes.
 template <int EPI, int BN>
 __global__ void __launch_bounds__(GemmGeo<BN>::NT) gemm_bf16(const bf16* __restrict__ A,
@@ -197,9 +198,9 @@ __global__ void __launch_bounds__(GemmGeo<BN>::NT) gemm_bf16(const bf16* __restr
 
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, gq = lane >> 4;
   const int wave = tid >> 6, wm = wave / G::NWN, wn = wave % G::NWN;
-  // global -> LDS: thread tid moves k-word tid % 4 of rows tid / 4 + RS j (A: kLA rows, B: kLB)
-  constexpr int RS = G::NT / 4;
-  const int r4 = tid >> 2, kc = 8 * (tid & 3);
+  // global -> LDS: thread tid moves k-word tid % 8 of rows tid / 8 + RS j (A: kLA rows, B: kLB)
+  constexpr int WPR = G::BK / 8, RS = G::NT / WPR;
+  const int r4 = tid / WPR, kc = 8 * (tid % WPR);
   const bf16* srcB = Bt + (int64_t)(n0 + r4) * K + kc;
   int64_t aoff[G::kLA];
 #pragma unroll
@@ -237,15 +238,20 @@ __global__ void __launch_bounds__(GemmGeo<BN>::NT) gemm_bf16(const bf16* __restr
       nb_[j] = *reinterpret_cast<const uint4*>(srcB + (int64_t)RS * j * K + kn);
     const bf16* cA = S + buf * G::STAGE + (64 * wm + l16) * G::LDK + 8 * gq;
     const bf16* cB = S + buf * G::STAGE + G::ASLAB + (64 * wn + l16) * G::LDK + 8 * gq;
-    uint4 fa[4], fb[4];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) fa[a] = *reinterpret_cast<const uint4*>(cA + 16 * a * G::LDK);
+    for (int kk = 0; kk < G::BK; kk += 32) {
+      uint4 fa[4], fb[4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) fb[b] = *reinterpret_cast<const uint4*>(cB + 16 * b * G::LDK);
+      for (int a = 0; a < 4; ++a)
+        fa[a] = *reinterpret_cast<const uint4*>(cA + 16 * a * G::LDK + kk);
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+      for (int b = 0; b < 4; ++b)
+        fb[b] = *reinterpret_cast<const uint4*>(cB + 16 * b * G::LDK + kk);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = mma_bf16(fa[a], fb[b], acc[a][b]);
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = mma_bf16(fa[a], fb[b], acc[a][b]);
+    }
     bf16* nS = S + (buf ^ 1) * G::STAGE;
 #pragma unroll
     for (int j = 0; j < G::kLA; ++j) *reinterpret_cast<uint4*>(nS + dA + RS * j * G::LDK) = na[j];
