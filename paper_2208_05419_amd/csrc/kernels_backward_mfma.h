@@ -25,15 +25,6 @@
 #include "kernels_mfma.h"
 
 namespace afno {
-// An opaque copy of a value: the compiler cannot tie expressions of the copy to expressions
-// of the original, so each phase of the column kernel derives its lane indices afresh instead
-// of keeping seven phases' worth of index arithmetic live (which spilled 35 VGPRs at 96 x 96).
-__device__ __forceinline__ int opq(int v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
-
-
 template <int HP, int BS>
 struct MfmaBwd {
   typedef MfmaCol<HP, BS> G;

@@ -34,6 +34,15 @@
 
 namespace afno {
 
+// An opaque copy of a value: expressions of the copy cannot be tied to expressions of the
+// original, so each product phase of a column kernel derives its lane indices afresh rather
+// than keeping every phase's index arithmetic live across the kernel.
+__device__ __forceinline__ int opq(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+
 // Geometry for padded height HP (H <= HP, HP a multiple of 32) and block size BS.
 template <int HP, int BS>
 struct MfmaCol {
@@ -134,7 +143,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
   extern __shared__ uint4 smem_mfma[];
   uint4* tab = smem_mfma;
   bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_mfma) + G::kTabBytes);
-  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63;  // the products take their own lane indices
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   const int blk = blockIdx.x % nb;  // consecutive workgroups -> different XCDs -> blocks
@@ -207,6 +216,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
 
   // ---- forward transform: Y^T = A(X) T -> tile Y[k][entry] (scaled by 1/sqrt(H) via T)
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
     __syncthreads();  // every wave has read its X fragments
@@ -232,6 +242,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
 
   // ---- layer 1 (transposed): H1^T[hidden][k] = relu(W1x^T Y^T + b1) -> tile H[k][hidden]
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
 #pragma unroll
     for (int m = 0; m < G::TMW; ++m)
@@ -290,6 +301,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
 
   // ---- layer 2: O[k][entry] = softshrink(H W2x + b2), cutoff -> planes O[rho][c][k]
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::LMW][G::LNW];
 #pragma unroll
     for (int m = 0; m < G::LMW; ++m)
@@ -356,6 +368,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
   // ---- inverse transform: Z^T = A'(O) T -> tile Z[h][entry] -> S rows h < H in 16-byte
   //      vectors (whole row segments per store instruction)
   {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 1, acc);
     __syncthreads();  // every wave has read its O fragments
