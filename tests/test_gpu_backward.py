@@ -141,3 +141,9 @@ def test_backward_nothing_kept_passes_gradient_through():
     assert np.array_equal(got["dx"], g)
     for k in ("dw1", "db1", "dw2", "db2"):
         assert not np.any(got[k])
+
+
+def test_backward_at_the_benchmark_configuration():
+    """The benchmark's backward: 90 x 180 x 768, 8 blocks of 96, bf16, B = 4, channel-scaled
+    fields (the weight gradients sum over the batch, so all four samples are compared)."""
+    _check(synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"], 2e-2)

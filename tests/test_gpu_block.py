@@ -65,3 +65,24 @@ def test_block_deterministic():
     b = afno.block_forward(x, p, 4, 0.01, 1.0)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_block_at_the_benchmark_configuration_sampled():
+    """The benchmark's block: 90 x 180 x 768, 8 blocks, B = 4, default parameters.  Samples
+    are independent through the block (the filter per sample, LayerNorm and the MLP per
+    token), so samples 0 and 3 are compared against the oracle run on those two alone."""
+    wl = synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"]
+    x_st = synth.make_x(wl, seed=0)
+    p_st = synth.make_block_params(wl, seed=0)
+    x = to_dev(x_st, "bf16")
+    p = {k: to_dev(v, "bf16") for k, v in p_st.items()}
+    out = afno.block_forward(x, p, wl.num_blocks, wl.lam, wl.keep)
+    torch.cuda.synchronize()
+    got = to_f64(out)[[0, 3]]
+    wide = {k: synth.widen(v, "bf16") for k, v in p_st.items()}
+    xs = synth.widen(x_st, "bf16")[[0, 3]]
+    ref = oblock.block_forward(xs, *(wide[k] for k in afno.BLOCK_PARAMS), wl.num_blocks, wl.lam,
+                               wl.keep)
+    e_out, e_d = max_rel(got, ref), max_rel(got - xs, ref - xs)
+    say(f"[block] benchmark configuration, samples 0 and 3: out {e_out:.2e}  out-x {e_d:.2e}")
+    assert e_out <= 2e-2 and e_d <= 2e-2

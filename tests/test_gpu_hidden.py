@@ -76,3 +76,20 @@ def test_hidden_equal_to_block_size_is_the_default_filter():
     torch.cuda.synchronize()
     assert rc == afno.AFNO_OK
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_hidden_at_the_benchmark_configuration_sampled():
+    """The benchmark's hidden-size workload (90 x 180 x 768, 8 blocks of 96, 192 hidden units,
+    B = 4, channel-scaled fields): samples are independent through the filter, so samples 0
+    and 3 are compared against the oracle run on those two alone."""
+    wl = synth.WORKLOADS["afno90x180_c768_nb8_hs192_bf16_b4"]
+    x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
+    w = dev_weights(w_st, "bf16")
+    out = afno.filter_forward(to_dev(x_st, "bf16"), w["w1"], w["b1"], w["w2"], w["b2"],
+                              wl.num_blocks, wl.lam, wl.keep)
+    torch.cuda.synchronize()
+    got = to_f64(out)[[0, 3]]
+    ref = oracle_run(x_st[[0, 3]], w_st, wl)
+    e_out = max_rel(got, ref)
+    say(f"[hidden] benchmark configuration, samples 0 and 3: out {e_out:.2e}")
+    assert e_out <= 2e-2
