@@ -210,3 +210,19 @@ def test_block_alias(kw):
 
 def test_block_empty_batch_is_ok_without_the_gpu():
     assert call_block(B=0, x=None, out=None) == afno.AFNO_OK
+
+
+def test_binding_rejects_mismatched_weight_shapes_before_any_gpu_call():
+    """filter_forward reads the hidden size from w1 and checks every weight shape first."""
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 4, 8, 32))
+    nb, bs, hs = 2, 16, 32
+    ok = dict(w1=torch.zeros((nb, bs, hs, 2)), b1=torch.zeros((nb, hs, 2)),
+              w2=torch.zeros((nb, hs, bs, 2)), b2=torch.zeros((nb, bs, 2)))
+    for bad in (dict(b1=torch.zeros((nb, bs, 2))), dict(w2=torch.zeros((nb, bs, bs, 2))),
+                dict(b2=torch.zeros((nb, hs, 2)))):
+        w = dict(ok, **bad)
+        with pytest.raises(ValueError, match="weight shapes"):
+            afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, 0.01)
+    with pytest.raises(ValueError, match="GPU"):  # well-formed, but host tensors
+        afno.filter_forward(x, ok["w1"], ok["b1"], ok["w2"], ok["b2"], nb, 0.01)
