@@ -155,9 +155,11 @@ int make_plan(const Args& a, afno::Plan& pl) {
   pl.spec_bytes = (size_t)a.B * a.H * pl.KW * a.C * 2 * es;
   pl.frag_offset = (pl.spec_bytes + 255) / 256 * 256;
   const bool mfma = afno::use_mfma_col(pl);
-  const size_t fb = (mfma || afno::use_fast_col(pl)) ? afno::frag_bytes(pl) : 0;
+  const bool hid = afno::use_mfma_hidden(pl);
+  const size_t fb = hid ? afno::hidden_frag_bytes(pl)
+                        : ((mfma || afno::use_fast_col(pl)) ? afno::frag_bytes(pl) : 0);
   pl.tab_offset = (pl.frag_offset + fb + 255) / 256 * 256;
-  pl.ws_bytes = mfma ? pl.tab_offset + afno::mfma_tab_bytes(pl) : pl.frag_offset + fb;
+  pl.ws_bytes = (mfma || hid) ? pl.tab_offset + afno::mfma_tab_bytes(pl) : pl.frag_offset + fb;
 
   // out must not overlap any input
   const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;

@@ -87,6 +87,8 @@ bool fast_col_available(int dtype, int64_t H, int64_t bs);
 bool mfma_col_available(int dtype, int64_t H, int64_t bs);
 bool use_mfma_col(const Plan& pl);  // under the current kernel path
 bool use_fast_col(const Plan& pl);  // under the current kernel path
+bool use_mfma_hidden(const Plan& pl);  // matrix-core column kernel for hidden = 2 bs
+size_t hidden_frag_bytes(const Plan& pl);
 size_t frag_bytes(const Plan& pl);
 size_t mfma_tab_bytes(const Plan& pl);
 // ev: NULL, or kProfEvents events recorded before the first kernel and after each phase

@@ -26,6 +26,7 @@
 #include "kernels_fast.h"
 #include "kernels_generic.h"
 #include "kernels_mfma.h"
+#include "kernels_hidden_mfma.h"
 #include "kernels_backward.h"
 #include "kernels_backward_mfma.h"
 #include "kernels_block.h"
@@ -160,6 +161,36 @@ static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* b1, const bf16*
 #undef AFNO_CASE
 }
 
+#define AFNO_MFMA_HID_LIST(X)                                                               \
+  X(32, 32, 64) X(32, 64, 128) X(32, 96, 192) X(64, 32, 64) X(64, 64, 128) X(64, 96, 192)   \
+  X(96, 32, 64) X(96, 64, 128) X(96, 96, 192)
+
+// the matrix-core column kernel for hidden = 2 bs (bf16, H <= 96, bs 32 / 64 / 96)
+static bool mfma_hidden_available(int dtype, int64_t H, int64_t bs, int64_t hs) {
+  return dtype == 1 && H <= 96 && (bs == 32 || bs == 64 || bs == 96) && hs == 2 * bs;
+}
+
+size_t hidden_frag_bytes(const Plan& pl) {
+  return (size_t)pl.nb * 2 * (size_t)(2 * pl.bs / 32) * (size_t)(2 * pl.col.hs / 16) * 64 * 16;
+}
+
+static void launch_col_mfma_hidden(const Plan& pl, bf16* S, const bf16* b1, const bf16* b2,
+                                   hipStream_t st) {
+  const uint4* wf = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.frag_offset);
+  const uint4* tab = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.tab_offset);
+  const int hp = mfma_col_hp(pl.H);
+  const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
+#define AFNO_CASE(HP_, BS_, HS_)                                                            \
+  if (hp == HP_ && pl.bs == BS_ && pl.col.hs == HS_) {                                      \
+    hipLaunchKernelGGL((column_mfma_hidden<HP_, BS_, HS_>), grid, dim3(512),                \
+                       (MfmaHid<HP_, BS_, HS_>::kBytes), st, S, wf, tab, b1, b2, (int)pl.H, \
+                       (int)pl.C, (int)pl.KW, (int)pl.nb, (int)pl.kept_h, pl.col.lam);       \
+    return;                                                                                 \
+  }
+  AFNO_MFMA_HID_LIST(AFNO_CASE)
+#undef AFNO_CASE
+}
+
 // ------------------------------------------------------------------ launchers
 
 // 0: MFMA-transform column kernel, else size-specialised, else generic; 1: generic only;
@@ -170,6 +201,11 @@ void set_kernel_path(int path) { g_kernel_path = path; }
 
 bool use_mfma_col(const Plan& pl) {
   return g_kernel_path == 0 && pl.col.hs == pl.bs && mfma_col_available(pl.dtype, pl.H, pl.bs);
+}
+
+bool use_mfma_hidden(const Plan& pl) {
+  return g_kernel_path == 0 && pl.col.hs != pl.bs &&
+         mfma_hidden_available(pl.dtype, pl.H, pl.bs, pl.col.hs);
 }
 
 bool use_fast_col(const Plan& pl) {
@@ -192,6 +228,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   const bool row_fast = !generic && fast_row_available(pl.W, pl.C);
   const bool col_mfma = use_mfma_col(pl);
   const bool col_fast = use_fast_col(pl);
+  const bool col_hid = use_mfma_hidden(pl);
   dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
   // prepared column-kernel operands (after the spectrum in the workspace; independent of x):
   // extra workgroups of the size-specialised W-axis forward launch, else a launch of their own
@@ -204,6 +241,17 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   if (pj.wout && !row_fast) {
     const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr) + 255) / 256, 4096);
     hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
+  }
+  if constexpr (sizeof(T) == 2) {
+    if (col_hid) {  // the hidden-size kernel's fragments and the DFT table, a launch of their own
+      const int hp = mfma_col_hp(pl.H);
+      const int64_t words = (int64_t)(hidden_frag_bytes(pl) + mfma_tab_bytes(pl)) / 16;
+      hipLaunchKernelGGL(prep_hidden_kernel, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 4096)),
+                         dim3(256), 0, st, static_cast<const bf16*>(w1), static_cast<const bf16*>(w2),
+                         reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.frag_offset),
+                         reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset),
+                         (int)pl.nb, (int)pl.bs, (int)pl.col.hs, (int)pl.H, hp);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -220,6 +268,9 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
     if constexpr (sizeof(T) == 2)
       launch_col_mfma(pl, St, static_cast<const bf16*>(b1), static_cast<const bf16*>(b2),
                       col_stage, st);
+  } else if (col_hid && col_stage == 0) {
+    if constexpr (sizeof(T) == 2)
+      launch_col_mfma_hidden(pl, St, static_cast<const bf16*>(b1), static_cast<const bf16*>(b2), st);
   } else if (col_fast)
     launch_col_fast<T>(pl, St, static_cast<const T*>(b1), static_cast<const T*>(b2), col_stage, st);
   else
@@ -529,6 +580,9 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 64, 3, 256>))
 #define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_mfma<HP_, BS_>))
   AFNO_MFMA_COL_LIST(AFNO_CASE)
+#undef AFNO_CASE
+#define AFNO_CASE(HP_, BS_, HS_) AFNO_ATTR((column_mfma_hidden<HP_, BS_, HS_>))
+  AFNO_MFMA_HID_LIST(AFNO_CASE)
 #undef AFNO_CASE
 #undef AFNO_ATTR
   return first;

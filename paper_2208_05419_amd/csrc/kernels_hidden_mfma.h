@@ -1,0 +1,301 @@
+// kernels_hidden_mfma.h -- the bf16 matrix-core column kernel for a block MLP whose hidden
+// size HS differs from the block size BS (the AFNO layer's hidden-size factor; the paper's
+// filter, "Model Innovations", has HS = BS and runs column_mfma).
+//
+// The same four products as column_mfma (forward DFT, the two layers, inverse DFT) in the same
+// geometry, except that the hidden layer H[k][hidden] (2 HS entries per row) has its own LDS
+// tile, layer 1 is computed in rounds of the forward kernel's tile count, and layer 2 runs over
+// K = 2 HS.  Weight fragments (prep_hidden_words): layer 1 as B fragments of W1x (K = 2 BS,
+// N = 2 HS), word (s MH + t) 64 + lane; then layer 2 as B fragments of W2x (K = 2 HS, N = 2 BS),
+// word L1 + (s MT + t) 64 + lane, with MH = 2 HS / 16, MT = 2 BS / 16, L1 = (2 BS / 32) MH 64.
+#pragma once
+#include "kernels_mfma.h"
+
+namespace afno {
+
+template <int HP, int BS, int HS>
+struct MfmaHid {
+  typedef MfmaCol<HP, BS> G;
+  static constexpr int MH = 2 * HS / 16;            // 16-entry tiles over the hidden layer
+  static constexpr int WKS2 = 2 * HS / 32;          // k-steps of layer 2
+  static constexpr int kRounds = MH / G::MT;        // layer-1 rounds of G::TMW tiles per wave
+  static constexpr int kLdh = 2 * HS + 8;           // hidden tile row stride (bf16)
+  static constexpr int kHBytes = HP * kLdh * 2;
+  static constexpr int64_t kL1Words = (int64_t)G::WKS * MH * 64;   // layer-1 fragment words
+  static constexpr int64_t kBlockWords = 2 * kL1Words;            // both layers
+  static constexpr int kBytes = G::kTabBytes + G::kRegionBytes + kHBytes;
+  static_assert(MH % G::MT == 0, "hidden tiles a multiple of the block's");
+};
+
+// fragment words of the hidden-size block weights (and, appended, the DFT table), i, i +
+// stride, ...: per block, layer 1 then layer 2 as described above
+__device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, const bf16* w1,
+                                                  const bf16* w2, uint4* wout, uint4* tout,
+                                                  int nb, int bs, int hs, int H, int HP) {
+  const int mh = 2 * hs / 16, mt = 2 * bs / 16;
+  const int64_t l1 = (int64_t)(2 * bs / 32) * mh * 64;
+  const int64_t per_block = 2 * l1;
+  const int64_t nw = (int64_t)nb * per_block;
+  const int64_t total = nw + (tout ? (int64_t)(2 * HP / 32) * (HP / 16) * 64 : 0);
+  for (; i < total; i += stride) {
+    if (i >= nw) {
+      tout[i - nw] = dft_table_word(i - nw, H, HP);
+      continue;
+    }
+    const int64_t blk = i / per_block;
+    int64_t u = i - blk * per_block;
+    const int layer = u >= l1 ? 1 : 0;
+    u -= layer * l1;
+    const int lane = (int)(u & 63);
+    const int64_t f = u >> 6;
+    const int nt = layer ? mt : mh;                 // output tiles of the layer
+    const int t = (int)(f % nt), s = (int)(f / nt);
+    const bf16* w = layer ? w2 + blk * (int64_t)hs * bs * 2 : w1 + blk * (int64_t)bs * hs * 2;
+    const int n_out = layer ? bs : hs;
+    const int j = (16 * t + (lane & 15)) >> 1;
+    wout[i] = FragWord<bf16>::make(w, n_out, s * 32, j, lane & 1, lane);
+  }
+}
+
+__global__ void __launch_bounds__(256) prep_hidden_kernel(const bf16* __restrict__ w1,
+                                                          const bf16* __restrict__ w2,
+                                                          uint4* __restrict__ wout,
+                                                          uint4* __restrict__ tout, int nb, int bs,
+                                                          int hs, int H, int HP) {
+  prep_hidden_words(blockIdx.x * (int64_t)blockDim.x + threadIdx.x,
+                    (int64_t)gridDim.x * blockDim.x, w1, w2, wout, tout, nb, bs, hs, H, HP);
+}
+
+// grid B * KW * nb (block index fastest), 512 threads, dynamic LDS MfmaHid<HP, BS, HS>::kBytes.
+// S: spectrum [B][H][KW][C] complex bf16, updated in place; wfrag, dtab from prep_hidden_kernel.
+template <int HP, int BS, int HS>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
+column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,
+                   const uint4* __restrict__ dtab, const bf16* __restrict__ b1,
+                   const bf16* __restrict__ b2, int H, int C, int KW, int nb, int kept_h,
+                   float lam) {
+  typedef MfmaCol<HP, BS> G;
+  typedef MfmaHid<HP, BS, HS> Q;
+  extern __shared__ uint4 smem_hid[];
+  uint4* tab = smem_hid;
+  bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_hid) + G::kTabBytes);
+  bf16* Hd = reinterpret_cast<bf16*>(reinterpret_cast<char*>(R) + G::kRegionBytes);
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int twm = wave / G::TWN, twn = wave % G::TWN;
+  const int lwm = wave / G::LWN, lwn = wave % G::LWN;
+
+  const int blk = blockIdx.x % nb;
+  const int rest = blockIdx.x / nb;
+  const int kw = rest % KW;
+  const int64_t b = rest / KW;
+  bf16* col = S + ((b * H) * KW + kw) * (int64_t)C * 2 + (int64_t)blk * BS * 2;
+  const uint32_t rsb = (uint32_t)KW * (uint32_t)C * 4;
+  const uint32_t cbytes = buf_bytes((uint64_t)H * rsb);
+  const Buf wb(wfrag + blk * Q::kBlockWords, (uint32_t)(Q::kBlockWords * 16));
+  constexpr uint32_t kL2Off = (uint32_t)(Q::kL1Words * 16);
+
+  // ---- the table and the column (planar planes X[rho][c][h], rows >= H zero)
+  for (int i = tid; i < G::kTabWords; i += G::kThreads) tab[i] = dtab[i];
+  {
+    const Buf cb(col, cbytes);
+    constexpr int XT = BS * (HP / 8);
+    constexpr int XR = (XT + G::kThreads - 1) / G::kThreads;
+    uint32_t xv[XR][8];
+#pragma unroll
+    for (int u = 0; u < XR; ++u) {
+      const int task = tid + u * G::kThreads;
+      const int c = task % BS, r0 = 8 * (task / BS);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = task < XT && r0 + e < H;
+        const uint32_t wv = cb.ld32(ok ? c * 4u + (uint32_t)(r0 + e) * rsb : 0u, 0);
+        xv[u][e] = ok ? wv : 0u;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < XR; ++u) {
+      const int task = tid + u * G::kThreads;
+      if (task < XT) {
+        const int c = task % BS, r0 = 8 * (task / BS);
+        uint4 re, im;
+        re.x = __builtin_amdgcn_perm(xv[u][1], xv[u][0], 0x05040100u);
+        re.y = __builtin_amdgcn_perm(xv[u][3], xv[u][2], 0x05040100u);
+        re.z = __builtin_amdgcn_perm(xv[u][5], xv[u][4], 0x05040100u);
+        re.w = __builtin_amdgcn_perm(xv[u][7], xv[u][6], 0x05040100u);
+        im.x = __builtin_amdgcn_perm(xv[u][1], xv[u][0], 0x07060302u);
+        im.y = __builtin_amdgcn_perm(xv[u][3], xv[u][2], 0x07060302u);
+        im.z = __builtin_amdgcn_perm(xv[u][5], xv[u][4], 0x07060302u);
+        im.w = __builtin_amdgcn_perm(xv[u][7], xv[u][6], 0x07060302u);
+        *reinterpret_cast<uint4*>(R + c * G::kLdx + r0) = re;
+        *reinterpret_cast<uint4*>(R + G::kPlane + c * G::kLdx + r0) = im;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- forward transform -> Y[k][entry]
+  {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+    f32x4 acc[G::TMW][G::TNW];
+    dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < G::TMW; ++m)
+#pragma unroll
+      for (int n = 0; n < G::TNW; ++n) {
+        const int k = 16 * (G::TNW * twn + n) + l16;
+        const int e0 = 16 * (G::TMW * twm + m) + 4 * g;
+        *reinterpret_cast<uint2*>(R + k * G::kLdy + e0) =
+            make_uint2(cvt_pk(acc[m][n][0], acc[m][n][1]), cvt_pk(acc[m][n][2], acc[m][n][3]));
+      }
+  }
+  __syncthreads();
+
+  // ---- layer 1 (transposed), in rounds: H^T[hidden][k] = relu(W1x^T Y^T + b1) -> Hd[k][hidden]
+#pragma unroll 1
+  for (int rd = 0; rd < Q::kRounds; ++rd) {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+    const int t0 = G::MT * rd + G::TMW * twm;  // first hidden tile of the wave this round
+    const uint32_t wvoff = lane * 16u;
+    auto wload = [&](int s, int t) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, wvoff,
+                                                          (uint32_t)((s * Q::MH + t) * 64 * 16), 0);
+      return make_uint4(v[0], v[1], v[2], v[3]);
+    };
+    f32x4 acc[G::TMW][G::TNW];
+#pragma unroll
+    for (int m = 0; m < G::TMW; ++m)
+#pragma unroll
+      for (int n = 0; n < G::TNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 wa[G::TMW];
+#pragma unroll
+    for (int m = 0; m < G::TMW; ++m) wa[m] = wload(0, t0 + m);
+#pragma unroll
+    for (int s = 0; s < G::WKS; ++s) {
+      uint4 wn_[G::TMW], yb[G::TNW];
+      if (s + 1 < G::WKS) {
+#pragma unroll
+        for (int m = 0; m < G::TMW; ++m) wn_[m] = wload(s + 1, t0 + m);
+      }
+#pragma unroll
+      for (int n = 0; n < G::TNW; ++n) {
+        const int k = 16 * (G::TNW * twn + n) + l16;
+        yb[n] = *reinterpret_cast<const uint4*>(R + k * G::kLdy + 32 * s + 8 * g);
+      }
+#pragma unroll
+      for (int m = 0; m < G::TMW; ++m)
+#pragma unroll
+        for (int n = 0; n < G::TNW; ++n) acc[m][n] = mma_bf16(wa[m], yb[n], acc[m][n]);
+      if (s + 1 < G::WKS) {
+#pragma unroll
+        for (int m = 0; m < G::TMW; ++m) wa[m] = wn_[m];
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < G::TMW; ++m) {
+      const int j0 = 16 * (t0 + m) + 4 * g;  // hidden entry of the lane's first row
+      const uint32_t* bp = reinterpret_cast<const uint32_t*>(b1 + (int64_t)blk * HS * 2 + j0);
+      const uint2 bb = make_uint2(bp[0], bp[1]);
+      const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
+                             __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+#pragma unroll
+      for (int n = 0; n < G::TNW; ++n) {
+        const int k = 16 * (G::TNW * twn + n) + l16;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[m][n][r] + bias[r], 0.f);
+        *reinterpret_cast<uint2*>(Hd + k * Q::kLdh + j0) =
+            make_uint2(cvt_pk(v[0], v[1]), cvt_pk(v[2], v[3]));
+      }
+    }
+  }
+  __syncthreads();  // the hidden layer complete; Y no longer read
+
+  // ---- layer 2: O[k][entry] = softshrink(H W2x + b2), cutoff -> planes O[rho][c][k] in R
+  {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+    const uint32_t wvoff = lane * 16u;
+    auto wload = [&](int s, int t) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, wvoff,
+                                                          kL2Off + (uint32_t)((s * G::MT + t) * 64 * 16), 0);
+      return make_uint4(v[0], v[1], v[2], v[3]);
+    };
+    f32x4 acc[G::LMW][G::LNW];
+#pragma unroll
+    for (int m = 0; m < G::LMW; ++m)
+#pragma unroll
+      for (int n = 0; n < G::LNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 wb_[G::LNW];
+#pragma unroll
+    for (int n = 0; n < G::LNW; ++n) wb_[n] = wload(0, G::LNW * lwn + n);
+#pragma unroll
+    for (int s = 0; s < Q::WKS2; ++s) {
+      uint4 wn_[G::LNW], ha[G::LMW];
+      if (s + 1 < Q::WKS2) {
+#pragma unroll
+        for (int n = 0; n < G::LNW; ++n) wn_[n] = wload(s + 1, G::LNW * lwn + n);
+      }
+#pragma unroll
+      for (int m = 0; m < G::LMW; ++m) {
+        const int k = 16 * (G::LMW * lwm + m) + l16;
+        ha[m] = *reinterpret_cast<const uint4*>(Hd + k * Q::kLdh + 32 * s + 8 * g);
+      }
+#pragma unroll
+      for (int m = 0; m < G::LMW; ++m)
+#pragma unroll
+        for (int n = 0; n < G::LNW; ++n) acc[m][n] = mma_bf16(ha[m], wb_[n], acc[m][n]);
+      if (s + 1 < Q::WKS2) {
+#pragma unroll
+        for (int n = 0; n < G::LNW; ++n) wb_[n] = wn_[n];
+      }
+    }
+    float bias[G::LNW];
+#pragma unroll
+    for (int n = 0; n < G::LNW; ++n) bias[n] = (float)b2[(int64_t)blk * BS * 2 + 16 * (G::LNW * lwn + n) + l16];
+    const bool all_rows = kept_h > H / 2;
+#pragma unroll
+    for (int m = 0; m < G::LMW; ++m) {
+      const int k0 = 16 * (G::LMW * lwm + m) + 4 * g;
+      bool keep[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) keep[r] = all_rows || row_kept(k0 + r, H, kept_h);
+#pragma unroll
+      for (int n = 0; n < G::LNW; ++n) {
+        const int e = 16 * (G::LNW * lwn + n) + l16;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = keep[r] ? softshrink(acc[m][n][r] + bias[n], lam) : 0.f;
+        *reinterpret_cast<uint2*>(R + (e & 1) * G::kPlane + (e >> 1) * G::kLdx + k0) =
+            make_uint2(cvt_pk(v[0], v[1]), cvt_pk(v[2], v[3]));
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- inverse transform -> Z[h][entry] -> S rows h < H
+  {
+    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+    f32x4 acc[G::TMW][G::TNW];
+    dft_product<HP, BS>(R, tab, lane, twm, twn, 1, acc);
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < G::TMW; ++m)
+#pragma unroll
+      for (int n = 0; n < G::TNW; ++n) {
+        const int h = 16 * (G::TNW * twn + n) + l16;
+        const int e0 = 16 * (G::TMW * twm + m) + 4 * g;
+        *reinterpret_cast<uint2*>(R + h * G::kLdy + e0) =
+            make_uint2(cvt_pk(acc[m][n][0], acc[m][n][1]), cvt_pk(acc[m][n][2], acc[m][n][3]));
+      }
+  }
+  __syncthreads();
+  constexpr int VPR = 2 * BS / 8;
+  const Buf cb(col, cbytes);
+  for (int it = tid; it < H * VPR; it += G::kThreads) {
+    const int h = it / VPR, cv = it - h * VPR;
+    cb.st128(*reinterpret_cast<const uint4*>(R + h * G::kLdy + cv * 8), cv * 16u + h * rsb, 0);
+  }
+}
+
+}  // namespace afno

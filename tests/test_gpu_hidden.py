@@ -1,6 +1,8 @@
 """GPU parity of the block MLP with a hidden size other than the block size
-(afno_filter_forward_hidden, the size-generic column kernel) against the float64 oracle,
-whose hidden size comes from the weights' shapes.
+(afno_filter_forward_hidden) against the float64 oracle, whose hidden size comes from the
+weights' shapes.  bf16 columns with H <= 96, block size 32, 64 or 96 and hidden = 2 bs run the
+matrix-core hidden-size kernel under the automatic path; everything else, and every case
+under the generic path, runs the size-generic column kernel.
 
 Bars as the forward's: fp32 1e-4 on out and on the filter's delta out - x (out is float32,
 so out - x is exact to ~1e-6 of the delta's scale); bf16 2e-2 on out, with weights of std 0.1
@@ -34,14 +36,37 @@ CASES = [
     (1, 90, 180, 768, 8, 192, "bf16", 0.01, 1.0, 0.1),     # hidden factor 2 at 90 x 180
     (2, 25, 30, 96, 2, 96, "bf16", 0.01, 0.6, 0.1),
     (1, 1, 2, 32, 1, 64, "bf16", 0.01, 1.0, 0.1),
+    # the matrix-core hidden-size kernel: each padded height and block size, ragged H, cutoff
+    (2, 64, 40, 128, 2, 128, "bf16", 0.01, 0.7, 0.1),      # bs 64, H = HP = 64
+    (1, 36, 20, 192, 2, 192, "bf16", 0.01, 1.0, 0.1),      # bs 96, HP 64, ragged
+    (3, 18, 10, 64, 2, 64, "bf16", 0.02, 0.5, 0.1),        # bs 32, HP 32, cutoff
+    (1, 96, 8, 96, 1, 192, "bf16", 0.01, 0.8, 0.1),        # bs 96, H = HP = 96
+    (2, 72, 12, 128, 4, 64, "bf16", 0.01, 1.0, 0.1),       # bs 32, HP 96
 ]
 
 
+def _mfma_case(H, C, nb, hs, dtype):
+    bs = C // nb
+    return dtype == "bf16" and H <= 96 and bs in (32, 64, 96) and hs == 2 * bs
+
+
+@pytest.mark.parametrize("path", ["auto", "generic"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_H{}_W{}_C{}_nb{}_hs{}_{}_k{}".format(*c[:9]))
-def test_hidden_parity(case):
+def test_hidden_parity(case, path):
     B, H, W, C, nb, hs, dtype, lam, keep, wstd = case
+    if path == "generic" and not _mfma_case(H, C, nb, hs, dtype):
+        pytest.skip("the automatic path already runs the generic kernel")
     wl = synth.Workload("hidden", B, H, W, C, nb, dtype, lam, keep, weight_std=wstd, hidden=hs)
-    say(f"[hidden] B={B} {H}x{W}x{C} nb={nb} bs={C // nb} hidden={hs} {dtype} keep={keep}")
+    say(f"[hidden] B={B} {H}x{W}x{C} nb={nb} bs={C // nb} hidden={hs} {dtype} keep={keep} {path}")
+    afno.set_kernel_path(afno.AFNO_PATH_AUTO if path == "auto" else afno.AFNO_PATH_GENERIC)
+    try:
+        _check_case(wl)
+    finally:
+        afno.set_kernel_path(afno.AFNO_PATH_AUTO)
+
+
+def _check_case(wl):
+    lam, keep, nb, dtype = wl.lam, wl.keep, wl.num_blocks, wl.dtype
     x_st, w_st = synth.make_x(wl, seed=3), synth.make_weights(wl, seed=3)
     w = dev_weights(w_st, dtype)
     x = to_dev(x_st, dtype)
