@@ -3,9 +3,11 @@
 // filter, "Model Innovations", has HS = BS and runs column_mfma).
 //
 // The same four products as column_mfma (forward DFT, the two layers, inverse DFT) in the same
-// geometry, except that the hidden layer H[k][hidden] (2 HS entries per row) has its own LDS
-// tile, layer 1 is computed in rounds of the forward kernel's tile count, and layer 2 runs over
-// K = 2 HS.  Weight fragments (prep_hidden_words): layer 1 as B fragments of W1x (K = 2 BS,
+// geometry, with the hidden layer taken in chunks of 2 BS entries: layer 1 writes one chunk
+// H_c[k][entry] to LDS, layer 2 adds H_c W2x[chunk rows] to accumulators held in registers
+// across the chunks.  The chunk tile occupies the table's LDS between the two transforms and
+// the table is loaded again for the inverse, so the kernel needs no more LDS than column_mfma
+// and two workgroups share a CU.  Weight fragments (prep_hidden_words): layer 1 as B fragments of W1x (K = 2 BS,
 // N = 2 HS), word (s MH + t) 64 + lane; then layer 2 as B fragments of W2x (K = 2 HS, N = 2 BS),
 // word L1 + (s MT + t) 64 + lane, with MH = 2 HS / 16, MT = 2 BS / 16, L1 = (2 BS / 32) MH 64.
 #pragma once
@@ -17,13 +19,14 @@ template <int HP, int BS, int HS>
 struct MfmaHid {
   typedef MfmaCol<HP, BS> G;
   static constexpr int MH = 2 * HS / 16;            // 16-entry tiles over the hidden layer
-  static constexpr int WKS2 = 2 * HS / 32;          // k-steps of layer 2
-  static constexpr int kRounds = MH / G::MT;        // layer-1 rounds of G::TMW tiles per wave
-  static constexpr int kLdh = 2 * HS + 8;           // hidden tile row stride (bf16)
-  static constexpr int kHBytes = HP * kLdh * 2;
+  static constexpr int kChunks = MH / G::MT;        // hidden chunks of 2 BS entries
   static constexpr int64_t kL1Words = (int64_t)G::WKS * MH * 64;   // layer-1 fragment words
   static constexpr int64_t kBlockWords = 2 * kL1Words;            // both layers
-  static constexpr int kBytes = G::kTabBytes + G::kRegionBytes + kHBytes;
+  // the hidden chunk [k][entry] shares the row-major stride of the spectrum tile and, once
+  // the forward transform is done, the table's LDS (the table is read again for the inverse)
+  static constexpr int kChunkBytes = HP * G::kLdy * 2;
+  static constexpr int kShared = ((G::kTabBytes > kChunkBytes ? G::kTabBytes : kChunkBytes) + 15) / 16 * 16;
+  static constexpr int kBytes = kShared + G::kRegionBytes;
   static_assert(MH % G::MT == 0, "hidden tiles a multiple of the block's");
 };
 
@@ -78,8 +81,8 @@ column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,
   typedef MfmaHid<HP, BS, HS> Q;
   extern __shared__ uint4 smem_hid[];
   uint4* tab = smem_hid;
-  bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_hid) + G::kTabBytes);
-  bf16* Hd = reinterpret_cast<bf16*>(reinterpret_cast<char*>(R) + G::kRegionBytes);
+  bf16* Hc = reinterpret_cast<bf16*>(smem_hid);  // the hidden chunk, over the table
+  bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_hid) + Q::kShared);
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int twm = wave / G::TWN, twn = wave % G::TWN;
@@ -139,7 +142,7 @@ column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,
     const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
     dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
-    __syncthreads();
+    __syncthreads();  // X and the table read
 #pragma unroll
     for (int m = 0; m < G::TMW; ++m)
 #pragma unroll
@@ -152,104 +155,114 @@ column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,
   }
   __syncthreads();
 
-  // ---- layer 1 (transposed), in rounds: H^T[hidden][k] = relu(W1x^T Y^T + b1) -> Hd[k][hidden]
+  // ---- the MLP over hidden chunks: per chunk c, layer 1 (transposed)
+  //      H_c^T[hidden][k] = relu(W1x[:, chunk]^T Y^T + b1[chunk]) -> Hc[k][entry], then layer 2
+  //      acc2 += H_c W2x[chunk rows]
+  f32x4 acc2[G::LMW][G::LNW];
+#pragma unroll
+  for (int m = 0; m < G::LMW; ++m)
+#pragma unroll
+    for (int n = 0; n < G::LNW; ++n) acc2[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
-  for (int rd = 0; rd < Q::kRounds; ++rd) {
-    const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
-    const int t0 = G::MT * rd + G::TMW * twm;  // first hidden tile of the wave this round
-    const uint32_t wvoff = lane * 16u;
-    auto wload = [&](int s, int t) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, wvoff,
-                                                          (uint32_t)((s * Q::MH + t) * 64 * 16), 0);
-      return make_uint4(v[0], v[1], v[2], v[3]);
-    };
-    f32x4 acc[G::TMW][G::TNW];
-#pragma unroll
-    for (int m = 0; m < G::TMW; ++m)
-#pragma unroll
-      for (int n = 0; n < G::TNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint4 wa[G::TMW];
-#pragma unroll
-    for (int m = 0; m < G::TMW; ++m) wa[m] = wload(0, t0 + m);
-#pragma unroll
-    for (int s = 0; s < G::WKS; ++s) {
-      uint4 wn_[G::TMW], yb[G::TNW];
-      if (s + 1 < G::WKS) {
-#pragma unroll
-        for (int m = 0; m < G::TMW; ++m) wn_[m] = wload(s + 1, t0 + m);
-      }
-#pragma unroll
-      for (int n = 0; n < G::TNW; ++n) {
-        const int k = 16 * (G::TNW * twn + n) + l16;
-        yb[n] = *reinterpret_cast<const uint4*>(R + k * G::kLdy + 32 * s + 8 * g);
-      }
+  for (int ch = 0; ch < Q::kChunks; ++ch) {
+    {
+      const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+      const int t0 = G::MT * ch + G::TMW * twm;  // the wave's first hidden tile of the chunk
+      const uint32_t wvoff = lane * 16u;
+      auto wload = [&](int s, int t) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, wvoff,
+                                                            (uint32_t)((s * Q::MH + t) * 64 * 16), 0);
+        return make_uint4(v[0], v[1], v[2], v[3]);
+      };
+      f32x4 acc[G::TMW][G::TNW];
 #pragma unroll
       for (int m = 0; m < G::TMW; ++m)
 #pragma unroll
-        for (int n = 0; n < G::TNW; ++n) acc[m][n] = mma_bf16(wa[m], yb[n], acc[m][n]);
-      if (s + 1 < G::WKS) {
+        for (int n = 0; n < G::TNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 wa[G::TMW];
 #pragma unroll
-        for (int m = 0; m < G::TMW; ++m) wa[m] = wn_[m];
+      for (int m = 0; m < G::TMW; ++m) wa[m] = wload(0, t0 + m);
+#pragma unroll
+      for (int s = 0; s < G::WKS; ++s) {
+        uint4 wn_[G::TMW], yb[G::TNW];
+        if (s + 1 < G::WKS) {
+#pragma unroll
+          for (int m = 0; m < G::TMW; ++m) wn_[m] = wload(s + 1, t0 + m);
+        }
+#pragma unroll
+        for (int n = 0; n < G::TNW; ++n) {
+          const int k = 16 * (G::TNW * twn + n) + l16;
+          yb[n] = *reinterpret_cast<const uint4*>(R + k * G::kLdy + 32 * s + 8 * g);
+        }
+#pragma unroll
+        for (int m = 0; m < G::TMW; ++m)
+#pragma unroll
+          for (int n = 0; n < G::TNW; ++n) acc[m][n] = mma_bf16(wa[m], yb[n], acc[m][n]);
+        if (s + 1 < G::WKS) {
+#pragma unroll
+          for (int m = 0; m < G::TMW; ++m) wa[m] = wn_[m];
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < G::TMW; ++m) {
+        const int jc = 16 * (G::TMW * twm + m) + 4 * g;  // entry within the chunk
+        const uint32_t* bp =
+            reinterpret_cast<const uint32_t*>(b1 + (int64_t)blk * HS * 2 + 2 * BS * ch + jc);
+        const uint2 bb = make_uint2(bp[0], bp[1]);
+        const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
+                               __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+#pragma unroll
+        for (int n = 0; n < G::TNW; ++n) {
+          const int k = 16 * (G::TNW * twn + n) + l16;
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[m][n][r] + bias[r], 0.f);
+          *reinterpret_cast<uint2*>(Hc + k * G::kLdy + jc) =
+              make_uint2(cvt_pk(v[0], v[1]), cvt_pk(v[2], v[3]));
+        }
       }
     }
+    __syncthreads();  // the chunk complete
+    {
+      const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
+      const uint32_t wvoff = lane * 16u;
+      auto wload = [&](int s, int t) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+            wb.r, wvoff, kL2Off + (uint32_t)(((G::WKS * ch + s) * G::MT + t) * 64 * 16), 0);
+        return make_uint4(v[0], v[1], v[2], v[3]);
+      };
+      uint4 wb_[G::LNW];
 #pragma unroll
-    for (int m = 0; m < G::TMW; ++m) {
-      const int j0 = 16 * (t0 + m) + 4 * g;  // hidden entry of the lane's first row
-      const uint32_t* bp = reinterpret_cast<const uint32_t*>(b1 + (int64_t)blk * HS * 2 + j0);
-      const uint2 bb = make_uint2(bp[0], bp[1]);
-      const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
-                             __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+      for (int n = 0; n < G::LNW; ++n) wb_[n] = wload(0, G::LNW * lwn + n);
 #pragma unroll
-      for (int n = 0; n < G::TNW; ++n) {
-        const int k = 16 * (G::TNW * twn + n) + l16;
-        float v[4];
+      for (int s = 0; s < G::WKS; ++s) {
+        uint4 wn_[G::LNW], ha[G::LMW];
+        if (s + 1 < G::WKS) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[m][n][r] + bias[r], 0.f);
-        *reinterpret_cast<uint2*>(Hd + k * Q::kLdh + j0) =
-            make_uint2(cvt_pk(v[0], v[1]), cvt_pk(v[2], v[3]));
+          for (int n = 0; n < G::LNW; ++n) wn_[n] = wload(s + 1, G::LNW * lwn + n);
+        }
+#pragma unroll
+        for (int m = 0; m < G::LMW; ++m) {
+          const int k = 16 * (G::LMW * lwm + m) + l16;
+          ha[m] = *reinterpret_cast<const uint4*>(Hc + k * G::kLdy + 32 * s + 8 * g);
+        }
+#pragma unroll
+        for (int m = 0; m < G::LMW; ++m)
+#pragma unroll
+          for (int n = 0; n < G::LNW; ++n) acc2[m][n] = mma_bf16(ha[m], wb_[n], acc2[m][n]);
+        if (s + 1 < G::WKS) {
+#pragma unroll
+          for (int n = 0; n < G::LNW; ++n) wb_[n] = wn_[n];
+        }
       }
     }
+    __syncthreads();  // the chunk read (and, after the last, Y no longer needed)
   }
-  __syncthreads();  // the hidden layer complete; Y no longer read
 
-  // ---- layer 2: O[k][entry] = softshrink(H W2x + b2), cutoff -> planes O[rho][c][k] in R
+  // ---- softshrink(acc2 + b2), cutoff -> planes O[rho][c][k] in R; the table back over the chunk
   {
     const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
-    const uint32_t wvoff = lane * 16u;
-    auto wload = [&](int s, int t) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(wb.r, wvoff,
-                                                          kL2Off + (uint32_t)((s * G::MT + t) * 64 * 16), 0);
-      return make_uint4(v[0], v[1], v[2], v[3]);
-    };
-    f32x4 acc[G::LMW][G::LNW];
-#pragma unroll
-    for (int m = 0; m < G::LMW; ++m)
-#pragma unroll
-      for (int n = 0; n < G::LNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint4 wb_[G::LNW];
-#pragma unroll
-    for (int n = 0; n < G::LNW; ++n) wb_[n] = wload(0, G::LNW * lwn + n);
-#pragma unroll
-    for (int s = 0; s < Q::WKS2; ++s) {
-      uint4 wn_[G::LNW], ha[G::LMW];
-      if (s + 1 < Q::WKS2) {
-#pragma unroll
-        for (int n = 0; n < G::LNW; ++n) wn_[n] = wload(s + 1, G::LNW * lwn + n);
-      }
-#pragma unroll
-      for (int m = 0; m < G::LMW; ++m) {
-        const int k = 16 * (G::LMW * lwm + m) + l16;
-        ha[m] = *reinterpret_cast<const uint4*>(Hd + k * Q::kLdh + 32 * s + 8 * g);
-      }
-#pragma unroll
-      for (int m = 0; m < G::LMW; ++m)
-#pragma unroll
-        for (int n = 0; n < G::LNW; ++n) acc[m][n] = mma_bf16(ha[m], wb_[n], acc[m][n]);
-      if (s + 1 < Q::WKS2) {
-#pragma unroll
-        for (int n = 0; n < G::LNW; ++n) wb_[n] = wn_[n];
-      }
-    }
+    for (int i = opq((int)threadIdx.x); i < G::kTabWords; i += G::kThreads) tab[i] = dtab[i];
     float bias[G::LNW];
 #pragma unroll
     for (int n = 0; n < G::LNW; ++n) bias[n] = (float)b2[(int64_t)blk * BS * 2 + 16 * (G::LNW * lwn + n) + l16];
@@ -265,7 +278,7 @@ column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,
         const int e = 16 * (G::LNW * lwn + n) + l16;
         float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = keep[r] ? softshrink(acc[m][n][r] + bias[n], lam) : 0.f;
+        for (int r = 0; r < 4; ++r) v[r] = keep[r] ? softshrink(acc2[m][n][r] + bias[n], lam) : 0.f;
         *reinterpret_cast<uint2*>(R + (e & 1) * G::kPlane + (e >> 1) * G::kLdx + k0) =
             make_uint2(cvt_pk(v[0], v[1]), cvt_pk(v[2], v[3]));
       }
