@@ -92,7 +92,9 @@ int afno_filter_forward(const void* x, const void* w1, const void* b1, const voi
  *   hidden > 0 (AFNO_ERR_INVALID_ARG otherwise); a multiple of 16 and <= 256, and the
  *   column's hidden layer (H x hidden complex values) must fit in LDS beside the column
  *   tile (AFNO_ERR_UNSUPPORTED otherwise).  hidden == bs runs exactly afno_filter_forward.
- * Other arguments, ownership and errors as afno_filter_forward.  hidden != bs runs the
+ * Other arguments, ownership and errors as afno_filter_forward.  hidden == 2 * bs with bf16
+ * storage, H <= 96 and bs 32, 64 or 96 runs a matrix-core column kernel (the workspace holds
+ * its weight fragments and the DFT table besides the spectrum); other hidden sizes run the
  * size-generic column kernel.
  */
 int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, const void* w2,
