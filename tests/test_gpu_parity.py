@@ -226,6 +226,10 @@ EDGE = [
     (1, 60, 32, 128, 2, "bf16", 0.01, 1.0),
     (2, 1, 4, 64, 2, "bf16", 0.01, 1.0),
     (1, 2, 6, 32, 1, "bf16", 0.01, 1.0),
+    # more padded-height-96 shapes: odd H, block size 96 with two blocks, block size 32
+    (1, 81, 10, 96, 1, "bf16", 0.01, 0.7),
+    (2, 72, 8, 192, 2, "bf16", 0.01, 1.0),
+    (1, 80, 6, 64, 2, "bf16", 0.01, 1.0),
     # H = 180 columns with the size-specialised vector-ALU transform kernels at block
     # sizes 32 (fp32 and bf16) and 64 (bf16), with and without a cutoff
     (1, 180, 24, 64, 2, "fp32", 0.01, 1.0),
