@@ -206,12 +206,14 @@ int afno_profile_end(double* kernel_ms, int64_t* calls);
  * specialised kernels where the library has them and the size-generic kernels elsewhere:
  * W-axis kernels for W in {32, 180, 360}; for bf16 with H <= 96 and bs in {32, 64, 96}
  * the column kernel that computes the H-axis DFTs as bf16 matrix-core products against a
- * DFT table; else column kernels with vector-ALU FFTs for H x bs in {16 x 16, 90 x 96,
- * 180 x 128 (bf16)}.  AFNO_PATH_VALU_DFT is AUTO without the matrix-core DFT column
- * kernel; AFNO_PATH_GENERIC runs the size-generic kernels for every shape.  All compute
- * the same filter (the matrix-core DFT rounds its table to bf16: one more bf16-sized
- * error per H transform).  Returns AFNO_OK or AFNO_ERR_INVALID_ARG.  Not for use while
- * calls are being enqueued from other threads.
+ * DFT table (and its hidden-size variant for hidden = 2 bs); else column kernels with
+ * vector-ALU FFTs for H x bs in {16 x 16, 90 x 96, 180 x 32, and for bf16 180 x 64 and
+ * 180 x 128}.  AFNO_PATH_VALU_DFT is AUTO without the matrix-core DFT column kernels;
+ * AFNO_PATH_GENERIC runs the size-generic kernels for every shape.  All compute the same
+ * filter (the matrix-core DFT rounds its table to bf16: one more bf16-sized error per H
+ * transform).  Returns AFNO_OK or AFNO_ERR_INVALID_ARG.  Safe while other threads enqueue
+ * calls: a call reads the setting once, when it sizes its workspace, and runs that path
+ * throughout.
  */
 enum { AFNO_PATH_AUTO = 0, AFNO_PATH_GENERIC = 1, AFNO_PATH_VALU_DFT = 2 };
 int afno_set_kernel_path(int path);

@@ -68,6 +68,7 @@ struct Args {
 // Validation (no HIP call) and plan construction.  Returns AFNO_OK, or an error code
 // with g_last_error set.
 int make_plan(const Args& a, afno::Plan& pl) {
+  pl.path = afno::kernel_path();
   if (a.dtype != AFNO_DTYPE_FP32 && a.dtype != AFNO_DTYPE_BF16)
     return fail(AFNO_ERR_INVALID_ARG, "dtype must be AFNO_DTYPE_FP32 (0) or AFNO_DTYPE_BF16 (1)");
   if (a.B < 0 || a.H <= 0 || a.W <= 0 || a.C <= 0 || a.nb <= 0)

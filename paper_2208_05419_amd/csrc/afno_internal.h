@@ -47,6 +47,7 @@ struct ColParams {
 struct Plan {
   int64_t B, H, W, C, nb, bs;
   int dtype;          // 0 fp32, 1 bf16
+  int path;           // kernel path (set_kernel_path) when the plan was made
   int64_t KW;         // kept_w: W columns that carry kept modes
   int64_t kept_h;
   RowParams row;
@@ -82,6 +83,7 @@ hipError_t set_kernel_attributes();
 // 0: specialised kernels where available, 1: generic only, 2: as 0 without the
 // MFMA-transform column kernel
 void set_kernel_path(int path);
+int kernel_path();
 bool fast_row_available(int64_t W, int64_t C);
 bool fast_col_available(int dtype, int64_t H, int64_t bs);
 bool mfma_col_available(int dtype, int64_t H, int64_t bs);

@@ -20,6 +20,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "afno_internal.h"
@@ -194,22 +195,24 @@ static void launch_col_mfma_hidden(const Plan& pl, bf16* S, const bf16* b1, cons
 // ------------------------------------------------------------------ launchers
 
 // 0: MFMA-transform column kernel, else size-specialised, else generic; 1: generic only;
-// 2: as 0 without the MFMA-transform column kernel
-static int g_kernel_path = 0;
+// 2: as 0 without the MFMA-transform column kernel.  A plan takes the value once (make_plan),
+// so a call's workspace sizing and its launches agree even if another thread switches it.
+static std::atomic<int> g_kernel_path{0};
 
-void set_kernel_path(int path) { g_kernel_path = path; }
+void set_kernel_path(int path) { g_kernel_path.store(path); }
+int kernel_path() { return g_kernel_path.load(); }
 
 bool use_mfma_col(const Plan& pl) {
-  return g_kernel_path == 0 && pl.col.hs == pl.bs && mfma_col_available(pl.dtype, pl.H, pl.bs);
+  return pl.path == 0 && pl.col.hs == pl.bs && mfma_col_available(pl.dtype, pl.H, pl.bs);
 }
 
 bool use_mfma_hidden(const Plan& pl) {
-  return g_kernel_path == 0 && pl.col.hs != pl.bs &&
+  return pl.path == 0 && pl.col.hs != pl.bs &&
          mfma_hidden_available(pl.dtype, pl.H, pl.bs, pl.col.hs);
 }
 
 bool use_fast_col(const Plan& pl) {
-  return g_kernel_path != 1 && pl.col.hs == pl.bs && !use_mfma_col(pl) &&
+  return pl.path != 1 && pl.col.hs == pl.bs && !use_mfma_col(pl) &&
          fast_col_available(pl.dtype, pl.H, pl.bs);
 }
 
@@ -224,7 +227,7 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
                              int stage, hipStream_t st, hipEvent_t* ev) {
   const T* xt = static_cast<const T*>(x);
   T* St = static_cast<T*>(S);
-  const bool generic = g_kernel_path == 1;
+  const bool generic = pl.path == 1;
   const bool row_fast = !generic && fast_row_available(pl.W, pl.C);
   const bool col_mfma = use_mfma_col(pl);
   const bool col_fast = use_fast_col(pl);
@@ -350,7 +353,7 @@ size_t bwd_acc_floats(const Plan& pl) {
 // The W-axis forward transform of x into S (no operand preparation).
 template <typename T>
 static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream_t st) {
-  if (g_kernel_path != 1 && fast_row_available(pl.W, pl.C)) {
+  if (pl.path != 1 && fast_row_available(pl.W, pl.C)) {
     PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0};
     launch_row_fwd_fast<T>(pl, x, S, pj, st);
   } else {
@@ -471,7 +474,7 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   // dx = g + C2R(Sg): the W-axis inverse with g as the residual
   T* dx = static_cast<T*>(a.dx);
-  if (g_kernel_path != 1 && fast_row_available(pl.W, pl.C))
+  if (pl.path != 1 && fast_row_available(pl.W, pl.C))
     launch_row_inv_fast<T>(pl, Sg, g, dx, nullptr, 0, st);
   else {
     dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
