@@ -405,14 +405,16 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   if (e == hipSuccess) e = launch_row_forward<T>(pl, g, Sg, st);
   if (e != hipSuccess) return e;
   const int64_t nw = (int64_t)2 * nb * bs * bs;
-  hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
-                     dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
-                     wt1, wt2, nb, bs);
   // cleared: the bias sums, and the products' sums where atomics accumulate them
   float* zero_from = nslab > 0 ? dbias : acc;
   const int64_t nzero = (int64_t)2 * nb * nb2 + (nslab > 0 ? 0 : nprod);
-  hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
-                     dim3(256), 0, st, zero_from, nzero);
+  if (!mfma) {
+    hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
+                       dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
+                       wt1, wt2, nb, bs);
+    hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
+                       dim3(256), 0, st, zero_from, nzero);
+  }
   if constexpr (sizeof(T) == 2) {
     if (mfma) {
       typedef typename FragWord<T>::type Word;
@@ -423,14 +425,17 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
                                                mfma_tab_bytes(pl));
       const int hp = mfma_col_hp(pl.H);
       const int64_t ntab = (int64_t)mfma_tab_bytes(pl) / 16;
-      hipLaunchKernelGGL(prep_dft_lo_kernel, dim3((unsigned)((ntab + 255) / 256)), dim3(256), 0, st,
-                         tab_lo, (int)pl.H, hp, ntab);
       PrepJob<T> pf{static_cast<const T*>(a.w1), static_cast<const T*>(a.w2), wfwd, tab, nb, bs,
                     (int)pl.H, hp, 0};
       PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0};
-      const unsigned gf = (unsigned)std::min<int64_t>((prep_words_host(pl, true) + 255) / 256, 4096);
+      // everything that does not read wt1 / wt2 in one launch, then their fragments
+      BwdPrep bp{pf, static_cast<const bf16*>(a.w1), static_cast<const bf16*>(a.w2), wt1, wt2,
+                 tab_lo, zero_from, nb, bs, (int)pl.H, hp, prep_words_host(pl, true), ntab, nw,
+                 nzero};
+      const int64_t nall = bp.n_pf + bp.n_lo + bp.n_ct + bp.n_zero;
+      hipLaunchKernelGGL(bwd_prep_kernel, dim3((unsigned)std::min<int64_t>((nall + 255) / 256, 4096)),
+                         dim3(256), 0, st, bp);
       const unsigned gb = (unsigned)std::min<int64_t>((prep_words_host(pl, false) + 255) / 256, 4096);
-      hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(gf), dim3(256), 0, st, pf);
       hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(gb), dim3(256), 0, st, pb);
       launch_col_bwd_mfma(pl, Sx, Sg, reinterpret_cast<const uint4*>(wfwd),
                           reinterpret_cast<const uint4*>(wbwd), tab, tab_lo,

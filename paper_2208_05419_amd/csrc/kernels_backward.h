@@ -31,22 +31,29 @@ namespace afno {
 
 // wt[k][j][i] = conj(w[k][i][j]) for both layers: x wt = x W^H on the block_gemm path
 template <typename T>
+__device__ __forceinline__ void conj_transpose_one(int64_t t, const T* __restrict__ w1,
+                                                   const T* __restrict__ w2, T* __restrict__ wt1,
+                                                   T* __restrict__ wt2, int nb, int bs) {
+  const int64_t n = (int64_t)nb * bs * bs;
+  const int layer = t >= n ? 1 : 0;
+  const int64_t u = t - layer * n;
+  const int64_t k = u / ((int64_t)bs * bs);
+  const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
+  const T* src = (layer ? w2 : w1) + ((k * bs + i) * bs + j) * 2;
+  T* dst = (layer ? wt2 : wt1) + ((k * bs + j) * bs + i) * 2;
+  dst[0] = src[0];
+  dst[1] = Store<T>::to(-ld_f(src + 1));
+}
+
+template <typename T>
 __global__ void __launch_bounds__(256) conj_transpose_weights(const T* __restrict__ w1,
                                                               const T* __restrict__ w2,
                                                               T* __restrict__ wt1,
                                                               T* __restrict__ wt2, int nb, int bs) {
   const int64_t n = (int64_t)nb * bs * bs;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
-       t += (int64_t)gridDim.x * blockDim.x) {
-    const int layer = t >= n ? 1 : 0;
-    const int64_t u = t - layer * n;
-    const int64_t k = u / ((int64_t)bs * bs);
-    const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
-    const T* src = (layer ? w2 : w1) + ((k * bs + i) * bs + j) * 2;
-    T* dst = (layer ? wt2 : wt1) + ((k * bs + j) * bs + i) * 2;
-    dst[0] = src[0];
-    dst[1] = Store<T>::to(-ld_f(src + 1));
-  }
+       t += (int64_t)gridDim.x * blockDim.x)
+    conj_transpose_one<T>(t, w1, w2, wt1, wt2, nb, bs);
 }
 
 template <typename T>

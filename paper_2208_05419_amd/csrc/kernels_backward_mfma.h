@@ -63,11 +63,34 @@ __device__ __forceinline__ uint4 dft_table_word_lo(int64_t i, int H, int HP) {
   return w.u;
 }
 
-__global__ void __launch_bounds__(256) prep_dft_lo_kernel(uint4* __restrict__ out, int H, int HP,
-                                                          int64_t nwords) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nwords;
-       i += (int64_t)gridDim.x * blockDim.x)
-    out[i] = dft_table_word_lo(i, H, HP);
+// The backward's independent preparations in one launch, index ranges in turn: the forward
+// operands (block weights in fragment order and the DFT table, PrepJob pf), the table's
+// rounding remainders, the conjugate-transposed weights, and the cleared sums.  The
+// fragments of the conjugate-transposed weights read wt1 / wt2 and follow in a launch of
+// their own.
+struct BwdPrep {
+  PrepJob<bf16> pf;
+  const bf16 *w1, *w2;
+  bf16 *wt1, *wt2;
+  uint4* tab_lo;
+  float* zero;
+  int nb, bs, H, HP;
+  int64_t n_pf, n_lo, n_ct, n_zero;
+};
+
+__global__ void __launch_bounds__(256) bwd_prep_kernel(BwdPrep p) {
+  const int64_t e1 = p.n_pf, e2 = e1 + p.n_lo, e3 = e2 + p.n_ct, e4 = e3 + p.n_zero;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < e4;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    if (t < e1)
+      prep_operands<bf16>(t, e4, p.pf);  // this word only (the next would be t + e4 >= e1)
+    else if (t < e2)
+      p.tab_lo[t - e1] = dft_table_word_lo(t - e1, p.H, p.HP);
+    else if (t < e3)
+      conj_transpose_one<bf16>(t - e2, p.w1, p.w2, p.wt1, p.wt2, p.nb, p.bs);
+    else
+      p.zero[t - e3] = 0.f;
+  }
 }
 
 // dft_product's sum accumulated onto acc, the table read from global memory (L2-resident)
