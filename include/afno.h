@@ -75,7 +75,9 @@ enum {
  * undefined.  AFNO_ERR_UNSUPPORTED: H or W not of the form 2^a 3^b 5^c, W odd,
  * bs not a multiple of 16 or above 128, or a grid too large for on-chip storage
  * (a column of H complex values x bs channels must fit the 160 KiB LDS of one CU,
- * H <= 192 for bs = 128, and W <= 1024).
+ * H <= 192 for bs = 128, and W <= 1024), or a spectrum column (H * kept_w * C complex
+ * values) or a grid row (W * C float32 values) larger than 4 GiB: the kernels address
+ * them with 32-bit byte offsets.
  * Thread safety: calls from several host threads are safe; calls whose streams
  * overlap in time only share read-only inputs.
  */
@@ -150,6 +152,20 @@ int afno_filter_stage(const void* x, const void* w1, const void* b1, const void*
                       const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
                       int64_t num_blocks, float lambda, float keep_fraction, int dtype,
                       int stage, float* dst, hipStream_t stream);
+
+/*
+ * afno_filter_stage_hidden -- afno_filter_stage for the block MLP with `hidden` units per
+ * block (weights as afno_filter_forward_hidden).  AFNO_STAGE_DELTA runs the same kernels as
+ * afno_filter_forward_hidden up to the inverse W-axis transform; AFNO_STAGE_SPECTRUM and
+ * AFNO_STAGE_MIXED stop inside the column pass, which for hidden != bs is the size-generic
+ * column kernel.  Arguments, ownership and errors as afno_filter_stage and
+ * afno_filter_forward_hidden (hidden <= 0: AFNO_ERR_INVALID_ARG).
+ */
+int afno_filter_stage_hidden(const void* x, const void* w1, const void* b1, const void* w2,
+                             const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                             int64_t num_blocks, int64_t hidden, float lambda,
+                             float keep_fraction, int dtype, int stage, float* dst,
+                             hipStream_t stream);
 
 /*
  * afno_filter_backward -- gradients of a loss L through out = x + filter(x), given

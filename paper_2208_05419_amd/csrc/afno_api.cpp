@@ -113,6 +113,17 @@ int make_plan(const Args& a, afno::Plan& pl) {
   const double elems = (double)a.B * a.H * a.W * a.C;
   if (elems > 4.0e15 || (double)a.B * a.H * (a.C / 16) > 2.0e9 || (double)a.B * Wm * a.nb > 2.0e9)
     return fail(AFNO_ERR_UNSUPPORTED, "tensor too large");
+  // the kernels address one column of the spectrum (H rows of kept_w * C complex values) and
+  // one row of the grid (W * C values, float32 for the diagnostic stage output) through
+  // 32-bit byte offsets from a per-workgroup base
+  {
+    const double col_span = (double)a.H * (double)pl.KW * (double)a.C * 2.0 * (double)es;
+    const double row_span = (double)a.W * (double)a.C * 4.0;
+    if (col_span > 4294967295.0 || row_span > 4294967295.0)
+      return fail(AFNO_ERR_UNSUPPORTED,
+                  "a spectrum column (H * kept_w * C complex values) or a grid row (W * C "
+                  "values) spans more than 4 GiB");
+  }
 
   // W-axis workgroups: rc channels, rc/2 complex signals
   pl.row.W = (int)a.W; pl.row.C = (int)a.C; pl.row.KW = (int)pl.KW;
@@ -408,6 +419,24 @@ int afno_filter_stage(const void* x, const void* w1, const void* b1, const void*
                                               : (size_t)B * H * (W / 2 + 1) * C * 2;
   Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, dst,
          B > 0 && H > 0 && W > 0 && C > 0 ? nd * sizeof(float) : 0};
+  return run(a, stage, dst, stream);
+}
+
+int afno_filter_stage_hidden(const void* x, const void* w1, const void* b1, const void* w2,
+                             const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                             int64_t num_blocks, int64_t hidden, float lambda,
+                             float keep_fraction, int dtype, int stage, float* dst,
+                             hipStream_t stream) {
+  g_last_error.clear();
+  if (hidden <= 0) return fail(AFNO_ERR_INVALID_ARG, "hidden must be > 0");
+  if (stage != AFNO_STAGE_SPECTRUM && stage != AFNO_STAGE_MIXED && stage != AFNO_STAGE_DELTA)
+    return fail(AFNO_ERR_INVALID_ARG, "stage must be AFNO_STAGE_SPECTRUM, _MIXED or _DELTA");
+  if (B > 0 && dst && !aligned(dst, 16))
+    return fail(AFNO_ERR_UNSUPPORTED, "dst must be 16-byte aligned");
+  const size_t nd = stage == AFNO_STAGE_DELTA ? (size_t)B * H * W * C
+                                              : (size_t)B * H * (W / 2 + 1) * C * 2;
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, dst,
+         B > 0 && H > 0 && W > 0 && C > 0 ? nd * sizeof(float) : 0, hidden};
   return run(a, stage, dst, stream);
 }
 

@@ -226,3 +226,112 @@ def test_binding_rejects_mismatched_weight_shapes_before_any_gpu_call():
             afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, 0.01)
     with pytest.raises(ValueError, match="GPU"):  # well-formed, but host tensors
         afno.filter_forward(x, ok["w1"], ok["b1"], ok["w2"], ok["b2"], nb, 0.01)
+
+
+def test_spectrum_column_span_beyond_32_bit_offsets_is_rejected():
+    """One column of the spectrum (H rows of kept_w * C complex values) must stay within the
+    kernels' 32-bit byte offsets: 90 x 91 x C x 4 bytes (bf16) crosses 2^32 between
+    C = 131072 and C = 132096 (block size 128)."""
+    bf = afno.AFNO_DTYPE_BF16
+    below = dict(H=90, W=180, C=131072, nb=1024, dtype=bf)
+    above = dict(H=90, W=180, C=132096, nb=1032, dtype=bf)
+    assert 90 * 91 * 131072 * 4 < 2 ** 32 <= 90 * 91 * 132096 * 4
+    assert call(**above) == afno.AFNO_ERR_UNSUPPORTED
+    assert "4 GiB" in afno.afno_last_error()
+    # below the limit the plan is accepted up to the last check (out overlapping x)
+    assert call(out=X, **below) == afno.AFNO_ERR_ALIAS
+    # keep < 1 shrinks the column: the same C then fits
+    assert call(out=X, keep=0.5, **above) == afno.AFNO_ERR_ALIAS
+
+
+def _host_weights(torch, nb, bs, hs, dtype):
+    return dict(w1=torch.zeros((nb, bs, hs, 2), dtype=dtype), b1=torch.zeros((nb, hs, 2), dtype=dtype),
+                w2=torch.zeros((nb, hs, bs, 2), dtype=dtype), b2=torch.zeros((nb, bs, 2), dtype=dtype))
+
+
+def test_binding_backward_rejects_a_hidden_size_other_than_the_block_size():
+    """The backward kernels run hidden = block size; weights of another hidden size would be
+    read (and gradients written) beyond their ends, so the binding refuses them first."""
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 4, 8, 192))
+    w = _host_weights(torch, 2, 96, 48, torch.float32)
+    with pytest.raises(ValueError, match="shape"):
+        afno.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], torch.zeros_like(x), 2, 0.01)
+    w = _host_weights(torch, 2, 96, 96, torch.float32)
+    with pytest.raises(ValueError, match="gout"):
+        afno.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], torch.zeros((1, 4, 8, 96)), 2,
+                             0.01)
+
+
+def test_binding_rejects_weights_of_another_dtype_or_device():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 4, 8, 32))
+    w = _host_weights(torch, 2, 16, 16, torch.bfloat16)   # fp32 x, bf16 weights
+    with pytest.raises(TypeError, match="dtype"):
+        afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], 2, 0.01)
+    with pytest.raises(TypeError, match="dtype"):
+        afno.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], torch.zeros_like(x), 2, 0.01)
+    xm = torch.zeros((1, 4, 8, 32), device="meta")     # weights on another device than x
+    w = _host_weights(torch, 2, 16, 16, torch.float32)
+    with pytest.raises(ValueError, match="device|meta"):
+        afno.filter_forward(xm, w["w1"], w["b1"], w["w2"], w["b2"], 2, 0.01)
+    with pytest.raises(ValueError, match="contiguous"):
+        wt = dict(w, w1=torch.zeros((2, 16, 16, 2)).transpose(1, 2))
+        afno.filter_forward(x, wt["w1"], wt["b1"], wt["w2"], wt["b2"], 2, 0.01)
+    with pytest.raises(ValueError, match="out"):
+        afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], 2, 0.01,
+                            out=torch.zeros((1, 4, 8, 16)))
+    with pytest.raises(ValueError, match="num_blocks"):
+        afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], 3, 0.01)
+    with pytest.raises(ValueError, match=r"\[B, H, W, C\]"):
+        afno.filter_forward(x[0], w["w1"], w["b1"], w["w2"], w["b2"], 2, 0.01)
+
+
+def test_binding_stage_checks_weights_and_takes_the_hidden_size_from_w1():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 4, 8, 32))
+    w = _host_weights(torch, 2, 16, 32, torch.float32)
+    with pytest.raises(ValueError, match="shape"):
+        afno.filter_stage(x, w["w1"], w["b2"], w["w2"], w["b2"], 2, 0.01, 1.0, afno.AFNO_STAGE_DELTA)
+    with pytest.raises(ValueError, match="GPU"):   # well-formed hidden weights, host tensors
+        afno.filter_stage(x, w["w1"], w["b1"], w["w2"], w["b2"], 2, 0.01, 1.0, afno.AFNO_STAGE_DELTA)
+
+
+def test_binding_block_checks_every_parameter_shape():
+    torch = pytest.importorskip("torch")
+    C, nb = 128, 4
+    x = torch.zeros((1, 4, 8, C), dtype=torch.bfloat16)
+    bf = torch.bfloat16
+    p = dict(_host_weights(torch, nb, C // nb, C // nb, bf))
+    p.update({k: torch.zeros(C, dtype=bf) for k in ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "bb")})
+    p.update(wa=torch.zeros((C, 4 * C), dtype=bf), ba=torch.zeros(4 * C, dtype=bf),
+             wb=torch.zeros((4 * C, C), dtype=bf))
+    for k, bad in (("wa", torch.zeros((4 * C, C), dtype=bf)), ("ba", torch.zeros(C, dtype=bf)),
+                   ("ln2_g", torch.zeros(C + 1, dtype=bf)), ("w1", torch.zeros((nb, 32, 64, 2), dtype=bf))):
+        with pytest.raises(ValueError, match=k):
+            afno.block_forward(x, dict(p, **{k: bad}), nb, 0.01)
+    with pytest.raises(TypeError, match="dtype"):
+        afno.block_forward(x, dict(p, bb=torch.zeros(C)), nb, 0.01)
+    with pytest.raises(ValueError, match="missing"):
+        afno.block_forward(x, {k: v for k, v in p.items() if k != "wb"}, nb, 0.01)
+    with pytest.raises(ValueError, match="GPU"):   # well-formed, host tensors
+        afno.block_forward(x, p, nb, 0.01)
+
+
+def call_stage_hidden(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, B=1, H=16, W=32, C=64, nb=4, hidden=32, lam=0.01,
+             keep=1.0, dtype=afno.AFNO_DTYPE_FP32, stage=afno.AFNO_STAGE_DELTA, dst=OUT)
+    a.update(kw)
+    return afno.afno_filter_stage_hidden(a["x"], a["w1"], a["b1"], a["w2"], a["b2"], a["B"],
+                                         a["H"], a["W"], a["C"], a["nb"], a["hidden"], a["lam"],
+                                         a["keep"], a["dtype"], a["stage"], a["dst"], None)
+
+
+def test_stage_hidden_validation():
+    assert call_stage_hidden(hidden=0) == afno.AFNO_ERR_INVALID_ARG
+    assert call_stage_hidden(stage=7) == afno.AFNO_ERR_INVALID_ARG
+    assert call_stage_hidden(hidden=24) == afno.AFNO_ERR_UNSUPPORTED
+    assert call_stage_hidden(dst=OUT + 8) == afno.AFNO_ERR_UNSUPPORTED
+    # w1 of the hidden size: 4 * 16 * 32 * 8 bytes = 16 KiB, so dst 8 KiB in overlaps it
+    assert call_stage_hidden(dst=W1 + 8192) == afno.AFNO_ERR_ALIAS
+    assert call_stage_hidden(B=0, x=None, dst=None) == afno.AFNO_OK
