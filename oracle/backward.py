@@ -93,7 +93,7 @@ def _round_c(z, rnd):
 
 
 def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: float,
-                    band: float = 0.0, decide: str = "exact"):
+                    band: float = 0.0, decide: str = "exact", flips=()):
     """Gradients of L with dL/dout = gout: returns dict dx [B,H,W,C], dw1, dw2 [nb,bs,bs,2],
     db1, db2 [nb,bs,2], all float64.
 
@@ -107,11 +107,13 @@ def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: 
 
     decide selects the precision of the two mask decisions (relu's v > 0, the softshrink's
     |o| > lam); the gradient values are float64 either way.  "exact": v and o in float64.
-    "bf16": v and o from bf16-stored intermediates, as a bf16-storage implementation forms
-    them: the W-axis spectrum, the 2-D spectrum X and the hidden layer h rounded to bf16
-    (products and sums then exact).  Near a kink a bf16 implementation decides on those
-    rounded operands; the decision itself is a step, so the comparison takes it in the
-    implementation's precision."""
+    "bf16" (a CPU diagnostic): v and o from bf16-stored intermediates, as a bf16-storage
+    implementation forms them: the W-axis spectrum, the 2-D spectrum X and the hidden layer h
+    rounded to bf16 (products and sums then exact).
+
+    flips: decisions to invert, each (kind, part, index) with kind "relu" (v > 0) or "soft"
+    (|o| > lam), part 0 (re) or 1 (im) and index (b, kh, kw, block, unit): the other branch at
+    an element that sits at a kink (see ambiguous_decisions)."""
     x = _f64(x)
     g = _f64(gout)
     B, H, W, C = x.shape
@@ -141,11 +143,20 @@ def filter_backward(x, w1, b1, w2, b2, gout, num_blocks: int, lam: float, keep: 
     else:
         raise ValueError(f"unknown decide {decide!r}")
 
+    # the two masks, with the requested decisions inverted
+    soft = [np.abs(o_dec.real) > lam, np.abs(o_dec.imag) > lam]
+    relu = [v_dec.real > 0, v_dec.imag > 0]
+    for kind, part, idx in flips:
+        if kind not in ("relu", "soft"):
+            raise ValueError(f"unknown decision kind {kind!r}")
+        m = relu if kind == "relu" else soft
+        m[part][tuple(idx)] = not m[part][tuple(idx)]
+
     # backward
     dz = (c[None, None, :, None] * rfft2(g)).reshape(B, H, Wm, nb, bs)
-    do = (dz.real * (np.abs(o_dec.real) > lam) + 1j * dz.imag * (np.abs(o_dec.imag) > lam)) * kept
+    do = (dz.real * soft[0] + 1j * dz.imag * soft[1]) * kept
     dh = _blocks(do, np.conj(W2).transpose(0, 2, 1))
-    dv = dh.real * (v_dec.real > 0) + 1j * dh.imag * (v_dec.imag > 0)
+    dv = dh.real * relu[0] + 1j * dh.imag * relu[1]
     dX = _blocks(dv, np.conj(W1).transpose(0, 2, 1))
     dw2 = _gram(np.conj(h), do)
     dw1 = _gram(np.conj(X), dv)
@@ -188,3 +199,34 @@ def _kink_allowance(X, v, h, o, dz, dh, kept, W1, W2, lam, band, hw):
             np.count_nonzero(a2i))
     return {"allow_dx": per_sample[:, None, None, :], "allow_dw1": both(dw1),
             "allow_db1": db1, "allow_dw2": both(dw2), "allow_db2": db2, "n_kinks": n}
+
+
+def ambiguous_decisions(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep: float,
+                        band: float):
+    """The decisions an implementation whose v and o are within band * rms(v) (band * rms(o))
+    of the exact float64 values may take either way: relu's at |v| <= band * rms(v) and the
+    softshrink's at ||o| - lam| <= band * rms(o), on kept modes, as flips entries (kind, part,
+    index) for filter_backward."""
+    x = _f64(x)
+    B, H, W, C = x.shape
+    nb = num_blocks
+    bs = C // nb
+    Wm = W // 2 + 1
+    lam = float(np.float32(lam))
+    keep = float(np.float32(keep))
+    W1, W2 = _cplx(w1), _cplx(w2)
+    B1, B2 = _cplx(b1), _cplx(b2)
+    X = rfft2(x).reshape(B, H, Wm, nb, bs)
+    v = _blocks(X, W1) + B1
+    h = np.maximum(v.real, 0.0) + 1j * np.maximum(v.imag, 0.0)
+    o = _blocks(h, W2) + B2
+    kept = np.broadcast_to(keep_mask(H, W, keep)[None, :, :, None, None], v.shape)
+    rms_v = np.sqrt(np.mean(v.real ** 2 + v.imag ** 2) / 2)
+    rms_o = np.sqrt(np.mean(o.real ** 2 + o.imag ** 2) / 2)
+    out = []
+    for part, (vp, op) in enumerate(((v.real, o.real), (v.imag, o.imag))):
+        for idx in zip(*np.nonzero((np.abs(vp) <= band * rms_v) & kept)):
+            out.append(("relu", part, tuple(int(i) for i in idx)))
+        for idx in zip(*np.nonzero((np.abs(np.abs(op) - lam) <= band * rms_o) & kept)):
+            out.append(("soft", part, tuple(int(i) for i in idx)))
+    return out

@@ -46,12 +46,13 @@ namespace afno {
 //   float one would not fit the LDS).
 int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
 
-// words of the preparation job: the fragment-ordered weights, and the DFT table if with_tab
-static int64_t prep_words_host(const Plan& pl, bool with_tab) {
+// tasks of the preparation job: the fragment-ordered weights' words, and the DFT table's
+// columns if with_tab
+static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h) {
   const int hp = mfma_col_hp(pl.H);
   return pl.nb * (pl.dtype == 0 ? frag_words_per_block<float>((int)pl.bs)
                                 : frag_words_per_block<bf16>((int)pl.bs)) +
-         (with_tab ? (int64_t)(2 * hp / 32) * (hp / 16) * 64 : 0);
+         (with_tab ? dft_table_tasks(hp, kept_h) : 0);
 }
 
 #define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
@@ -75,10 +76,11 @@ static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, PrepJob<T> pj,
 #define AFNO_CASE(w, n1, n2, np)                                                          \
   if (pl.W == w) {                                                                        \
     const unsigned nmain = (unsigned)row_grid<np, (int)sizeof(T)>(gx, (int)(pl.C / (2 * np))); \
-    pj.nmain = (int)nmain;                                                                \
-    const unsigned nprep = pj.wout ? (unsigned)std::min<int64_t>(                         \
-        (prep_words_host(pl, pj.tout != nullptr) + np * n1 - 1) / (np * n1), 1024) : 0;   \
-    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nmain + nprep),              \
+    const unsigned nprep = pj.wout ? (unsigned)(std::min<int64_t>(                        \
+        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h) + np * n1 - 1) / (np * n1), 1024) \
+        + 7) / 8 * 8 : 0;                                                                 \
+    pj.nprep = (int)nprep;                                                                \
+    hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nprep + nmain),              \
                        dim3(np * n1), 0, st, x, S, (int)pl.C, (int)pl.KW, sc, (int64_t)gx, pj); \
     return;                                                                               \
   }
@@ -236,24 +238,24 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   // prepared column-kernel operands (after the spectrum in the workspace; independent of x):
   // extra workgroups of the size-specialised W-axis forward launch, else a launch of their own
   PrepJob<T> pj{static_cast<const T*>(w1), static_cast<const T*>(w2), nullptr, nullptr,
-                (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0};
+                (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0, (int)pl.kept_h};
   if (col_mfma || col_fast)
     pj.wout = reinterpret_cast<typename FragWord<T>::type*>(static_cast<char*>(S) + pl.frag_offset);
   if (col_mfma) pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
   if (ev) (void)hipEventRecord(ev[0], st);
   if (pj.wout && !row_fast) {
-    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr) + 255) / 256, 4096);
+    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr, pj.kept_h) + 255) / 256, 4096);
     hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
   }
   if constexpr (sizeof(T) == 2) {
     if (col_hid) {  // the hidden-size kernel's fragments and the DFT table, a launch of their own
       const int hp = mfma_col_hp(pl.H);
-      const int64_t words = (int64_t)(hidden_frag_bytes(pl) + mfma_tab_bytes(pl)) / 16;
+      const int64_t words = (int64_t)hidden_frag_bytes(pl) / 16 + 2 * hp;
       hipLaunchKernelGGL(prep_hidden_kernel, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 4096)),
                          dim3(256), 0, st, static_cast<const bf16*>(w1), static_cast<const bf16*>(w2),
                          reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.frag_offset),
                          reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset),
-                         (int)pl.nb, (int)pl.bs, (int)pl.col.hs, (int)pl.H, hp);
+                         (int)pl.nb, (int)pl.bs, (int)pl.col.hs, (int)pl.H, hp, (int)pl.kept_h);
     }
   }
   hipError_t e = hipGetLastError();
@@ -354,7 +356,7 @@ size_t bwd_acc_floats(const Plan& pl) {
 template <typename T>
 static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream_t st) {
   if (pl.path != 1 && fast_row_available(pl.W, pl.C)) {
-    PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0};
+    PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0, -1};
     launch_row_fwd_fast<T>(pl, x, S, pj, st);
   } else {
     dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
@@ -425,17 +427,18 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
                                                mfma_tab_bytes(pl));
       const int hp = mfma_col_hp(pl.H);
       const int64_t ntab = (int64_t)mfma_tab_bytes(pl) / 16;
+      // the table rounded entry by entry (kept_h -1): tab_lo holds its remainders
       PrepJob<T> pf{static_cast<const T*>(a.w1), static_cast<const T*>(a.w2), wfwd, tab, nb, bs,
-                    (int)pl.H, hp, 0};
-      PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0};
+                    (int)pl.H, hp, 0, -1};
+      PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0, -1};
       // everything that does not read wt1 / wt2 in one launch, then their fragments
       BwdPrep bp{pf, static_cast<const bf16*>(a.w1), static_cast<const bf16*>(a.w2), wt1, wt2,
-                 tab_lo, zero_from, nb, bs, (int)pl.H, hp, prep_words_host(pl, true), ntab, nw,
+                 tab_lo, zero_from, nb, bs, (int)pl.H, hp, prep_words_host(pl, true, -1), ntab, nw,
                  nzero};
       const int64_t nall = bp.n_pf + bp.n_lo + bp.n_ct + bp.n_zero;
       hipLaunchKernelGGL(bwd_prep_kernel, dim3((unsigned)std::min<int64_t>((nall + 255) / 256, 4096)),
                          dim3(256), 0, st, bp);
-      const unsigned gb = (unsigned)std::min<int64_t>((prep_words_host(pl, false) + 255) / 256, 4096);
+      const unsigned gb = (unsigned)std::min<int64_t>((prep_words_host(pl, false, -1) + 255) / 256, 4096);
       hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(gb), dim3(256), 0, st, pb);
       launch_col_bwd_mfma(pl, Sx, Sg, reinterpret_cast<const uint4*>(wfwd),
                           reinterpret_cast<const uint4*>(wbwd), tab, tab_lo,

@@ -83,7 +83,7 @@ __global__ void __launch_bounds__(256) bwd_prep_kernel(BwdPrep p) {
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < e4;
        t += (int64_t)gridDim.x * blockDim.x) {
     if (t < e1)
-      prep_operands<bf16>(t, e4, p.pf);  // this word only (the next would be t + e4 >= e1)
+      prep_operands<bf16>(t, e4, p.pf, nullptr);  // this word only (the next: t + e4 >= e1)
     else if (t < e2)
       p.tab_lo[t - e1] = dft_table_word_lo(t - e1, p.H, p.HP);
     else if (t < e3)

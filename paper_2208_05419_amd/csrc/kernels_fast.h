@@ -153,27 +153,29 @@ __device__ __forceinline__ bool row_slice(int g, int nchunk, int64_t nrows, int6
 
 // ------------------------------------------------------------------ W-axis forward
 
-// grid row_grid(B H, C / (2 NP)) (= pj.nmain) + the workgroups of the appended preparation
-// job, block NP * N1.  NP complex signals (2 NP channels) per workgroup; signal p of thread
-// t = t % NP.
+// grid pj.nprep (a multiple of 8: the preparation job's workgroups, dispatched first so that
+// their longer tasks overlap the transforms) + row_grid(B H, C / (2 NP)), block NP * N1.  NP
+// complex signals (2 NP channels) per workgroup; signal p of thread t = t % NP.
 template <typename T, int W, int N1, int N2, int NP>
 __global__ void __launch_bounds__(NP * N1)
 row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float scale,
              int64_t nrows, PrepJob<T> pj) {
   static_assert(N1 * N2 == W && W % 2 == 0, "W = N1 N2, even");
+  static_assert(N2 * N1 * NP >= 96, "room for the table's roots");
   constexpr int NT = NP * N1;
-  if ((int)blockIdx.x >= pj.nmain) {  // appended workgroups: the column kernel's operands
-    prep_operands<T>((int64_t)(blockIdx.x - pj.nmain) * NT + threadIdx.x,
-                     (int64_t)(gridDim.x - pj.nmain) * NT, pj);
-    return;
-  }
   __shared__ float2 F[N2 * N1 * NP];
   __shared__ float2 tw[W];
+  if ((int)blockIdx.x < pj.nprep) {  // the column kernel's operands
+    if (pj.tout && pj.kept_h >= 0) dft_roots(F, pj.H);
+    prep_operands<T>((int64_t)blockIdx.x * NT + threadIdx.x, (int64_t)pj.nprep * NT, pj, F);
+    return;
+  }
   const int tid = threadIdx.x;
-  // the workgroup's row b H + h and channel slice
+  // the workgroup's row b H + h and channel slice (pj.nprep is a multiple of 8, so workgroup
+  // g keeps its XCD: consecutive workgroups go to consecutive XCDs)
   int64_t row;
   int c0;
-  if (!row_slice<NP, (int)sizeof(T)>(blockIdx.x, C / (2 * NP), nrows, row, c0)) return;
+  if (!row_slice<NP, (int)sizeof(T)>(blockIdx.x - pj.nprep, C / (2 * NP), nrows, row, c0)) return;
   constexpr uint32_t es = sizeof(T);
   const uint32_t xrow = (uint32_t)C * es;        // bytes between consecutive w
   const uint32_t srow = (uint32_t)C * 2 * es;    // bytes between consecutive kw of S

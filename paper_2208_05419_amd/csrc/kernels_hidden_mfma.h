@@ -30,19 +30,20 @@ struct MfmaHid {
   static_assert(MH % G::MT == 0, "hidden tiles a multiple of the block's");
 };
 
-// fragment words of the hidden-size block weights (and, appended, the DFT table), i, i +
-// stride, ...: per block, layer 1 then layer 2 as described above
+// fragment words of the hidden-size block weights (and, appended, the DFT table's 2 HP column
+// tasks, dft_table_column), i, i + stride, ...: per block, layer 1 then layer 2 as above
 __device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, const bf16* w1,
                                                   const bf16* w2, uint4* wout, uint4* tout,
-                                                  int nb, int bs, int hs, int H, int HP) {
+                                                  int nb, int bs, int hs, int H, int HP,
+                                                  int kept_h, const float2* roots) {
   const int mh = 2 * hs / 16, mt = 2 * bs / 16;
   const int64_t l1 = (int64_t)(2 * bs / 32) * mh * 64;
   const int64_t per_block = 2 * l1;
   const int64_t nw = (int64_t)nb * per_block;
-  const int64_t total = nw + (tout ? (int64_t)(2 * HP / 32) * (HP / 16) * 64 : 0);
+  const int64_t total = nw + (tout ? (int64_t)2 * HP : 0);
   for (; i < total; i += stride) {
     if (i >= nw) {
-      tout[i - nw] = dft_table_word(i - nw, H, HP);
+      dft_table_column((int)(i - nw), H, HP, kept_h, roots, tout);
       continue;
     }
     const int64_t blk = i / per_block;
@@ -64,9 +65,12 @@ __global__ void __launch_bounds__(256) prep_hidden_kernel(const bf16* __restrict
                                                           const bf16* __restrict__ w2,
                                                           uint4* __restrict__ wout,
                                                           uint4* __restrict__ tout, int nb, int bs,
-                                                          int hs, int H, int HP) {
+                                                          int hs, int H, int HP, int kept_h) {
+  __shared__ float2 roots[96];
+  dft_roots(roots, H);
   prep_hidden_words(blockIdx.x * (int64_t)blockDim.x + threadIdx.x,
-                    (int64_t)gridDim.x * blockDim.x, w1, w2, wout, tout, nb, bs, hs, H, HP);
+                    (int64_t)gridDim.x * blockDim.x, w1, w2, wout, tout, nb, bs, hs, H, HP, kept_h,
+                    roots);
 }
 
 // grid B * KW * nb (block index fastest), 512 threads, dynamic LDS MfmaHid<HP, BS, HS>::kBytes.

@@ -34,9 +34,67 @@ __device__ __forceinline__ uint4 dft_table_word(int64_t i, int H, int HP) {
   return w.u;
 }
 
+// The H-th roots of unity the transform table is made of: roots[m] = (cos, sin)(2 pi m / H),
+// m < H, computed by the workgroup's threads (the same single-precision sincospif values
+// dft_table_word takes).  Ends with a barrier: every thread of the workgroup must call it.
+__device__ __forceinline__ void dft_roots(float2* roots, int H) {
+  for (int m = threadIdx.x; m < H; m += blockDim.x) {
+    float sn, cs;
+    sincospif(2.0f * (float)m / (float)H, &sn, &cs);
+    roots[m] = make_float2(cs, sn);
+  }
+  __syncthreads();
+}
+
+// One column (sigma, j) of the transform table: T[(sigma, r)][j] for every r < HP, each entry
+// stored at its place in dft_table_word's fragment order (2-byte stores), from the roots of
+// dft_roots.  The matrix-core column kernels apply this one table in both directions, and the
+// inverse's sum over the kept rows k of T[(sigma, k)][h] O[k] meets a component of O that is
+// the same at every kept row (the biases put one there, tens of times the rest): with each
+// entry rounded to the nearest bf16 on its own, that component carries the column's summed
+// rounding error (about sqrt(H) half-ulps) onto every output row h instead of row 0 alone.  So
+// the entries of the kept rows (|signed r| < kept_h, every row when kept_h > H / 2) are
+// rounded in turn with the error carried forward: entry r takes the bf16 nearest to v_r - e,
+// e the sum of the earlier entries' errors, which keeps every partial column sum within half
+// an ulp of its exact value while each entry stays within about one ulp of v_r.
+__device__ __forceinline__ void dft_table_column(int task, int H, int HP, int kept_h,
+                                                 const float2* roots, uint4* tout) {
+  const int sigma = task / HP, j = task - sigma * HP;
+  const int KT = HP / 16;
+  bf16* tb = reinterpret_cast<bf16*>(tout);
+  const float sc = 1.0f / sqrtf((float)H);
+  const bool all_rows = kept_h > H / 2;
+  float err = 0.f;
+  for (int r0 = 0; r0 < HP; r0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int r = r0 + e;
+      v[e] = 0.f;
+      if (r < H && j < H) {
+        const float2 z = roots[(r * j) % H];
+        v[e] = sigma == 0 ? z.x * sc : -z.y * sc;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int r = r0 + e;
+      const bool carry = r < H && (all_rows || row_kept(r, H, kept_h));
+      const bf16 b = (bf16)(carry ? v[e] - err : v[e]);
+      if (carry) err += (float)b - v[e];
+      const int kap = sigma * HP + r;  // K row of the real-ified table
+      const int64_t word =
+          ((int64_t)(kap >> 5) * KT + (j >> 4)) * 64 + (j & 15) + 16 * ((kap >> 3) & 3);
+      tb[word * 8 + (kap & 7)] = b;
+    }
+  }
+}
+
 // What to prepare: both layers of every block in fragment order (frag_words_per_block words
 // per block, word ((layer * KSTEPS + s) * NT16 + t) * 64 + lane), then, if tout is set, the
-// DFT table for height H padded to HP.
+// DFT table for height H padded to HP: kept_h >= 0, 2 HP column tasks (dft_table_column, the
+// rounding that carries its error over the kept rows; needs dft_roots); kept_h < 0, one task
+// per fragment word (dft_table_word, every entry rounded to nearest).
 template <typename T>
 struct PrepJob {
   const T* w1;
@@ -44,24 +102,34 @@ struct PrepJob {
   typename FragWord<T>::type* wout;
   uint4* tout;
   int nb, bs, H, HP;
-  int nmain;  // workgroups of the host launch's own work (the prepared words come after)
+  int nprep;   // workgroups the host launch gives the job (placed before its own work)
+  int kept_h;  // the table's rounding, as above
 };
+
+__host__ __device__ inline int64_t dft_table_tasks(int HP, int kept_h) {
+  return kept_h >= 0 ? (int64_t)2 * HP : (int64_t)(2 * HP / 32) * (HP / 16) * 64;
+}
 
 template <typename T>
 __device__ __forceinline__ int64_t prep_words(const PrepJob<T>& pj) {
   return (int64_t)pj.nb * frag_words_per_block<T>(pj.bs) +
-         (pj.tout ? (int64_t)(2 * pj.HP / 32) * (pj.HP / 16) * 64 : 0);
+         (pj.tout ? dft_table_tasks(pj.HP, pj.kept_h) : 0);
 }
 
-// Words i, i + stride, ... of the job.
+// Tasks i, i + stride, ... of the job: one fragment word of the weights each, then the table
+// tasks.  roots: dft_roots' values (needed when pj.tout is set and pj.kept_h >= 0).
 template <typename T>
-__device__ void prep_operands(int64_t i, int64_t stride, const PrepJob<T>& pj) {
+__device__ void prep_operands(int64_t i, int64_t stride, const PrepJob<T>& pj,
+                              const float2* roots) {
   const int nt16 = 2 * pj.bs / 16, ksteps = 2 * pj.bs / Mma<T>::kK;
   const int64_t nw = (int64_t)pj.nb * frag_words_per_block<T>(pj.bs);
   const int64_t total = prep_words(pj);
   for (; i < total; i += stride) {
     if (i >= nw) {
-      pj.tout[i - nw] = dft_table_word(i - nw, pj.H, pj.HP);
+      if (pj.kept_h >= 0)
+        dft_table_column((int)(i - nw), pj.H, pj.HP, pj.kept_h, roots, pj.tout);
+      else
+        pj.tout[i - nw] = dft_table_word(i - nw, pj.H, pj.HP);
       continue;
     }
     const int lane = (int)(i & 63);
@@ -78,10 +146,13 @@ __device__ void prep_operands(int64_t i, int64_t stride, const PrepJob<T>& pj) {
   }
 }
 
-// The job as its own launch (grid-stride over the words).
+// The job as its own launch (grid-stride over the tasks).  H <= 96 when the table is made.
 template <typename T>
 __global__ void __launch_bounds__(256) prep_operands_kernel(PrepJob<T> pj) {
-  prep_operands<T>(blockIdx.x * (int64_t)blockDim.x + threadIdx.x, (int64_t)gridDim.x * blockDim.x, pj);
+  __shared__ float2 roots[96];
+  if (pj.tout && pj.kept_h >= 0) dft_roots(roots, pj.H);
+  prep_operands<T>(blockIdx.x * (int64_t)blockDim.x + threadIdx.x, (int64_t)gridDim.x * blockDim.x,
+                   pj, roots);
 }
 
 }  // namespace afno

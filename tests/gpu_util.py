@@ -45,3 +45,14 @@ def oracle_run(x_st, w_st, wl: synth.Workload, stages: bool = False):
 
 def dev_weights(w_st, dtype):
     return {k: to_dev(v, dtype) for k, v in w_st.items()}
+
+
+def off_row0_rel(g: np.ndarray, r: np.ndarray) -> float:
+    """max_rel over the rows h >= 1 of [B, H, W, C] arrays of the filter's delta.  The biases
+    add the same value at every kept mode, and the inverse transform of that constant is a
+    spike on row h = 0 which sets max |r| over the whole tensor (tens of times the rest), so
+    max_rel over everything barely sees the other rows; this metric is normalised by those
+    rows alone.  0 when H = 1."""
+    if g.shape[1] < 2:
+        return 0.0
+    return max_rel(g[:, 1:], r[:, 1:])

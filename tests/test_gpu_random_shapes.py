@@ -4,14 +4,15 @@ nobody listed by hand (odd heights beside even widths, block sizes beside padded
 cutoffs that keep one row or one column) run through whichever kernels the automatic path
 picks for them.  The draw is the same on every run (seed 2208); each case prints its shape.
 
-Bars as the other parity tests: out and the filter's delta (float32 stage output) within
-1e-4 (fp32 storage) or 2e-2 (bf16), metric max|g - r| / max|r|."""
+Bars as the other parity tests: out, the filter's delta (float32 stage output) and the
+delta's rows h >= 1 at their own scale within 1e-4 (fp32 storage) or 2e-2 (bf16), metric
+max|g - r| / max|r|."""
 import numpy as np
 import pytest
 
 import paper_2208_05419_amd as afno
 from paper_2208_05419_amd import synth
-from gpu_util import TOL, dev_weights, max_rel, oracle_run, say, to_dev, to_f64
+from gpu_util import TOL, dev_weights, max_rel, off_row0_rel, oracle_run, say, to_dev, to_f64
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -69,6 +70,8 @@ def test_random_shape(case):
     ref, st = oracle_run(x_st, w_st, wl, stages=True)
     e_out = max_rel(to_f64(out), ref)
     e_delta = max_rel(to_f64(delta), st["delta"])
-    say(f"  out rel {e_out:.3e}  delta rel {e_delta:.3e}  (tol {TOL[dtype]})")
+    e_rows = off_row0_rel(to_f64(delta), st["delta"])
+    say(f"  out rel {e_out:.3e}  delta rel {e_delta:.3e}  rows h>=1 {e_rows:.3e}  (tol {TOL[dtype]})")
     assert e_out <= TOL[dtype]
     assert e_delta <= TOL[dtype]
+    assert e_rows <= TOL[dtype]

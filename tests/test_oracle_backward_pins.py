@@ -3,6 +3,8 @@ central finite differences of the forward oracle (directional derivatives of
 L = <gout, out>), an independent float64 implementation differentiated by torch autograd
 (torch.fft's pocketfft transforms, which the forward pins tie to the same conventions), and
 the linear-regime closed form.  CPU only."""
+import itertools
+
 import numpy as np
 import pytest
 
@@ -180,3 +182,118 @@ def test_kink_allowance_bounds_decision_flips():
         moved += int(np.count_nonzero(d > 1e-12))
         assert np.all(d <= ref["allow_" + k] + 1e-12), k
     assert moved > 0 and ref["n_kinks"] > 0   # some decisions did flip
+
+
+def test_a_flipped_decision_equals_the_exact_gradient_just_across_the_kink():
+    """flips: b1 is moved so that the element of v nearest 0 sits at +-1e-9 (every other element
+    of that unit keeps its side, the nearest one being the only one the move brings closer);
+    inverting relu's decision there gives the gradients that the exact decisions give with that
+    element moved to -+1e-9, up to the O(1e-9) continuous change.  Same for the softshrink
+    decision nearest |o| = lam, through b2."""
+    rng = np.random.default_rng(21)
+    B, H, W, C, nb, lam = 1, 6, 8, 16, 2, 0.05
+    bs = C // nb
+    x = rng.standard_normal((B, H, W, C))
+    w = {"w1": rng.standard_normal((nb, bs, bs, 2)) * 0.3, "b1": rng.standard_normal((nb, bs, 2)) * 0.1,
+         "w2": rng.standard_normal((nb, bs, bs, 2)) * 0.3, "b2": rng.standard_normal((nb, bs, 2)) * 0.1}
+    g = rng.standard_normal(x.shape)
+    Wm = W // 2 + 1
+    X = oracle.rfft2(x).reshape(B, H, Wm, nb, bs)
+    cw = lambda a: a[..., 0] + 1j * a[..., 1]  # noqa: E731
+    eps = 1e-9
+
+    def run(b1, b2, flips=()):
+        return ob.filter_backward(x, w["w1"], b1, w["w2"], b2, g, nb, lam, 1.0, flips=flips)
+
+    v = np.einsum("bhwki,kij->bhwkj", X, cw(w["w1"])) + cw(w["b1"])
+    idx = np.unravel_index(np.argmin(np.abs(v.real)), v.shape)
+    sgn = np.sign(v.real[idx])
+    base = w["b1"].copy()
+    base[idx[3], idx[4], 0] += -v.real[idx] + sgn * eps
+    across = base.copy()
+    across[idx[3], idx[4], 0] -= 2 * sgn * eps
+    flipped = run(base, w["b2"], flips=[("relu", 0, idx)])
+    other = run(across, w["b2"])
+    plain = run(base, w["b2"])
+    for k in ("dx", "dw1", "db1", "dw2", "db2"):
+        scale = np.max(np.abs(plain[k]))
+        assert np.max(np.abs(flipped[k] - other[k])) <= 1e-6 * scale, k
+    assert max(np.max(np.abs(flipped[k] - plain[k])) / np.max(np.abs(plain[k]))
+               for k in ("dw1", "db1")) > 1e-4
+
+    # softshrink: the element of Im o nearest |o| = lam, moved through b2
+    h = np.maximum(v.real, 0) + 1j * np.maximum(v.imag, 0)
+    o = np.einsum("bhwkj,kjl->bhwkl", h, cw(w["w2"])) + cw(w["b2"])
+    d = np.abs(o.imag) - lam
+    idx = np.unravel_index(np.argmin(np.abs(d)), d.shape)
+    s_o = np.sign(o.imag[idx])
+    base = w["b2"].copy()   # |o| = lam + eps at idx (o keeps its sign)
+    base[idx[3], idx[4], 1] += s_o * (-d[idx] + eps)
+    across = base.copy()    # |o| = lam - eps
+    across[idx[3], idx[4], 1] -= s_o * 2 * eps
+    flipped = run(w["b1"], base, flips=[("soft", 1, idx)])
+    other = run(w["b1"], across)
+    plain = run(w["b1"], base)
+    for k in ("dx", "dw1", "db1", "dw2", "db2"):
+        scale = np.max(np.abs(plain[k]))
+        assert np.max(np.abs(flipped[k] - other[k])) <= 1e-6 * scale, k
+    assert max(np.max(np.abs(flipped[k] - plain[k])) / np.max(np.abs(plain[k]))
+               for k in ("dw2", "db2")) > 1e-4
+
+
+def test_ambiguous_decisions_lists_exactly_the_elements_in_the_band():
+    rng = np.random.default_rng(22)
+    B, H, W, C, nb, lam = 1, 5, 8, 16, 2, 0.05
+    bs = C // nb
+    x = rng.standard_normal((B, H, W, C))
+    w = {"w1": rng.standard_normal((nb, bs, bs, 2)) * 0.3, "b1": rng.standard_normal((nb, bs, 2)) * 0.1,
+         "w2": rng.standard_normal((nb, bs, bs, 2)) * 0.3, "b2": rng.standard_normal((nb, bs, 2)) * 0.1}
+    amb = ob.ambiguous_decisions(x, w["w1"], w["b1"], w["w2"], w["b2"], nb, lam, 0.7, 0.02)
+    Wm = W // 2 + 1
+    X = oracle.rfft2(x).reshape(B, H, Wm, nb, bs)
+    cw = lambda a: a[..., 0] + 1j * a[..., 1]  # noqa: E731
+    v = np.einsum("bhwki,kij->bhwkj", X, cw(w["w1"])) + cw(w["b1"])
+    h = np.maximum(v.real, 0) + 1j * np.maximum(v.imag, 0)
+    o = np.einsum("bhwkj,kjl->bhwkl", h, cw(w["w2"])) + cw(w["b2"])
+    kept = oracle.keep_mask(H, W, float(np.float32(0.7)))
+    rv = np.sqrt(np.mean(np.abs(v) ** 2) / 2)
+    ro = np.sqrt(np.mean(np.abs(o) ** 2) / 2)
+    want = set()
+    for b, a, c, k, j in itertools.product(range(B), range(H), range(Wm), range(nb), range(bs)):
+        if not kept[a, c]:
+            continue
+        for part, (vp, op) in enumerate(((v.real, o.real), (v.imag, o.imag))):
+            if abs(vp[b, a, c, k, j]) <= 0.02 * rv:
+                want.add(("relu", part, (b, a, c, k, j)))
+            if abs(abs(op[b, a, c, k, j]) - lam) <= 0.02 * ro:
+                want.add(("soft", part, (b, a, c, k, j)))
+    assert set(amb) == want and len(want) > 0
+
+
+@pytest.mark.parametrize("dtype,keep", [("bf16", 1.0), ("fp32", 0.6), ("bf16", 0.5)])
+def test_known_mask_inputs_leave_no_decision_near_a_kink(dtype, keep):
+    """choose_biases: with the returned b1, b2, lam no kept decision lies within the margins
+    (checked here with ambiguous_decisions, an independent listing), the biases are values of
+    the storage dtype, and the planted frequencies make some masks change between modes."""
+    from oracle import known_masks as km
+    from paper_2208_05419_amd import synth
+    wl = synth.Workload("km", 2, 12, 20, 64, 2, dtype, 0.01, keep)
+    rng = np.random.default_rng(5)
+    x = synth.widen(synth.make_x(wl), dtype)
+    w = {k: synth.widen(v, dtype) for k, v in synth.make_weights(wl).items()}
+    x, planted = km.plant_frequencies(x, dtype, keep, 3, 1.0, rng)
+    assert np.array_equal(synth.widen(synth.quantize(x, dtype), dtype), x)
+    b1, b2, lam, info = km.choose_biases(x, w["w1"], w["w2"], wl.num_blocks, keep, dtype, rng)
+    for b in (b1, b2):
+        assert np.array_equal(synth.widen(synth.quantize(b, dtype), dtype), b)
+    assert info["relu_mixed"] > 0.1 and info["softshrink_mixed"] > 0.05
+    Wm = wl.W // 2 + 1
+    X = oracle.rfft2(x).reshape(wl.B, wl.H, Wm, wl.num_blocks, wl.bs)
+    cw = lambda a: a[..., 0] + 1j * a[..., 1]  # noqa: E731
+    v = np.einsum("bhwki,kij->bhwkj", X, cw(w["w1"])) + cw(b1)
+    h = np.maximum(v.real, 0) + 1j * np.maximum(v.imag, 0)
+    o = np.einsum("bhwkj,kjl->bhwkl", h, cw(w["w2"])) + cw(b2)
+    rv = np.sqrt(np.mean(np.abs(v) ** 2) / 2)
+    ro = np.sqrt(np.mean(np.abs(o) ** 2) / 2)
+    band = 0.999 * min(info["m1"] / rv, info["m2"] / ro)
+    assert ob.ambiguous_decisions(x, w["w1"], b1, w["w2"], b2, wl.num_blocks, lam, keep, band) == []
