@@ -87,6 +87,28 @@ int afno_filter_forward(const void* x, const void* w1, const void* b1, const voi
                         void* out, hipStream_t stream);
 
 /*
+ * afno_filter_forward_noalloc -- afno_filter_forward for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, kernels and result (bitwise) as afno_filter_forward; the call allocates
+ * nothing.  Its workspace (the spectrum, B*H*kept_w*C complex values of 4 bytes (bf16) or 8
+ * (fp32), then the prepared block weights and the DFT table, about 1.2 MB for 8 blocks of 96)
+ * is an array of AFNO_NOALLOC_MAX_WORKSPACE bytes in device memory that the library holds on
+ * every GPU it runs on until the process ends (the 90 x 180 x 768 bf16 filter fits up to
+ * B = 5).  AFNO_ERR_UNSUPPORTED, before any HIP call, when the workspace would be larger.
+ * Every call on a GPU uses that GPU's one array, which keeps the last call's contents (each
+ * call writes all it reads): calls whose work overlaps in time on one GPU (different streams
+ * or host threads without ordering between them) race and leave out undefined; calls on one
+ * stream are ordered and safe.  The first call on a device also resolves the array's address
+ * there (hipGetSymbolAddress; AFNO_ERR_HIP if that fails).  Other errors as
+ * afno_filter_forward.
+ */
+#define AFNO_NOALLOC_MAX_WORKSPACE (128u << 20)
+int afno_filter_forward_noalloc(const void* x, const void* w1, const void* b1, const void* w2,
+                                const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                                int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                                void* out, hipStream_t stream);
+
+/*
  * afno_filter_forward_hidden -- the same filter with `hidden` hidden units per block in
  * the block MLP (the AFNO layer's hidden-size factor: hidden = factor * bs; the paper's
  * filter, "Model Innovations", uses hidden = bs, which afno_filter_forward assumes).

@@ -10,6 +10,7 @@ from .afno import (AFNO_DTYPE_BF16, AFNO_DTYPE_FP32, AFNO_ERR_ALIAS, AFNO_ERR_HI
                    AFNO_PATH_GENERIC, AFNO_PATH_VALU_DFT, AFNO_STAGE_DELTA,
                    AFNO_STAGE_MIXED, AFNO_STAGE_SPECTRUM, EXPORTED, LIB_PATH, AfnoError,
                    BLOCK_PARAMS, KERNELS, afno_block_forward, afno_filter_backward, afno_filter_forward, afno_filter_forward_hidden,
+                   afno_filter_forward_noalloc, filter_forward_noalloc,
                    afno_filter_stage, afno_filter_stage_hidden,
                    afno_last_error, afno_profile_begin, afno_profile_end, afno_set_kernel_path,
                    afno_version, block_forward, filter_backward, filter_forward, filter_stage,

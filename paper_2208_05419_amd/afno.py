@@ -27,7 +27,8 @@ AFNO_PATH_AUTO = 0
 AFNO_PATH_GENERIC = 1
 AFNO_PATH_VALU_DFT = 2
 
-EXPORTED = ("afno_filter_forward", "afno_filter_forward_hidden", "afno_block_forward",
+EXPORTED = ("afno_filter_forward", "afno_filter_forward_noalloc", "afno_filter_forward_hidden",
+            "afno_block_forward",
             "afno_filter_stage", "afno_filter_stage_hidden", "afno_filter_backward",
             "afno_profile_begin", "afno_profile_end", "afno_set_kernel_path", "afno_last_error",
             "afno_version")
@@ -65,6 +66,9 @@ def load_library():
     lib.afno_filter_forward.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32, f32,
                                         ctypes.c_int, vp, vp]
     lib.afno_filter_forward.restype = ctypes.c_int
+    lib.afno_filter_forward_noalloc.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, f32,
+                                                f32, ctypes.c_int, vp, vp]
+    lib.afno_filter_forward_noalloc.restype = ctypes.c_int
     lib.afno_filter_forward_hidden.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                                f32, f32, ctypes.c_int, vp, vp]
     lib.afno_filter_forward_hidden.restype = ctypes.c_int
@@ -113,6 +117,13 @@ def afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fra
     """Raw call: pointers as ints (or None), returns the C return code."""
     return load_library().afno_filter_forward(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam,
                                               keep_fraction, dtype, out, stream)
+
+
+def afno_filter_forward_noalloc(x, w1, b1, w2, b2, B, H, W, C, num_blocks, lam, keep_fraction,
+                                dtype, out, stream) -> int:
+    """Raw call of the allocation-free variant: pointers as ints (or None)."""
+    return load_library().afno_filter_forward_noalloc(x, w1, b1, w2, b2, B, H, W, C, num_blocks,
+                                                      lam, keep_fraction, dtype, out, stream)
 
 
 def afno_filter_forward_hidden(x, w1, b1, w2, b2, B, H, W, C, num_blocks, hidden, lam,
@@ -275,6 +286,20 @@ def filter_forward(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction
                                         C, num_blocks, hs, lam, keep_fraction, _dtype_code(x),
                                         _ptr(out), _stream(stream))
     _check(rc)
+    return out
+
+
+def filter_forward_noalloc(x, w1, b1, w2, b2, num_blocks: int, lam: float, keep_fraction: float,
+                           out, stream=None):
+    """afno_filter_forward_noalloc: out = x + AFNO filter(x) into the caller's out, with no
+    device allocation (the library's fixed workspace; hidden size = block size).  Calls that
+    overlap in time on one GPU race (see include/afno.h)."""
+    (B, H, W, C, bs, hs), specs = _filter_specs(x, w1, b1, w2, b2, num_blocks, False)
+    specs.append(("out", out, tuple(x.shape), None))
+    _expect(x, specs)
+    _check(afno_filter_forward_noalloc(_ptr(x), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), B, H, W,
+                                       C, num_blocks, lam, keep_fraction, _dtype_code(x),
+                                       _ptr(out), _stream(stream)))
     return out
 
 

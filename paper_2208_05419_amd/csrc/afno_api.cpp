@@ -187,6 +187,41 @@ int make_plan(const Args& a, afno::Plan& pl) {
 
 std::once_flag g_attr_once;
 
+// The workspace of afno_filter_forward_noalloc: a file-scope device array, one copy on every
+// GPU the library runs on, held until the process ends.  Its name in host code is only a
+// handle: scratch_address() resolves the current device's copy once and host code passes that
+// address on, never the name.
+constexpr size_t kScratchBytes = (size_t)AFNO_NOALLOC_MAX_WORKSPACE;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of scratch (hipGetSymbolAddress on the first call per device).
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AFNO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  }
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(AFNO_ERR_UNSUPPORTED, "device index beyond the library's table of devices");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return fail(AFNO_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return AFNO_OK;
+}
+
 // diagnostic per-kernel timing (afno_profile_begin / afno_profile_end)
 struct Profile {
   std::mutex mu;
@@ -202,10 +237,16 @@ hipEvent_t* profile_slot() {
   return &g_prof.ev[afno::kProfEvents * (size_t)g_prof.used++];
 }
 
-int run(const Args& a, int stage, float* dst, hipStream_t stream) {
+// noalloc: the workspace is the current device's scratch array (no allocation); a plan
+// whose workspace exceeds it is rejected before any HIP call.
+int run(const Args& a, int stage, float* dst, hipStream_t stream, bool noalloc = false) {
   afno::Plan pl;
   int rc = make_plan(a, pl);
   if (rc != AFNO_OK || a.B == 0) return rc;
+  if (noalloc && pl.KW > 0 && pl.ws_bytes > kScratchBytes)
+    return fail(AFNO_ERR_UNSUPPORTED, "the workspace of " + std::to_string(pl.ws_bytes) +
+                                          " bytes exceeds the " + std::to_string(kScratchBytes) +
+                                          " bytes of afno_filter_forward_noalloc");
 
   std::call_once(g_attr_once, [] {
     (void)afno::set_kernel_attributes();
@@ -227,6 +268,14 @@ int run(const Args& a, int stage, float* dst, hipStream_t stream) {
   }
 
   void* S = nullptr;
+  if (noalloc) {
+    rc = scratch_address(&S);
+    if (rc != AFNO_OK) return rc;
+    hipEvent_t* ev = stage == afno::kStageFull ? profile_slot() : nullptr;
+    e = afno::launch_filter(pl, a.x, a.w1, a.b1, a.w2, a.b2, S, a.out, dst, stage, stream, ev);
+    if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
+    return AFNO_OK;
+  }
   e = hipMallocAsync(&S, pl.ws_bytes, stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -382,6 +431,15 @@ int afno_filter_forward(const void* x, const void* w1, const void* b1, const voi
   g_last_error.clear();
   Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0};
   return run(a, afno::kStageFull, nullptr, stream);
+}
+
+int afno_filter_forward_noalloc(const void* x, const void* w1, const void* b1, const void* w2,
+                                const void* b2, int64_t B, int64_t H, int64_t W, int64_t C,
+                                int64_t num_blocks, float lambda, float keep_fraction, int dtype,
+                                void* out, hipStream_t stream) {
+  g_last_error.clear();
+  Args a{x, w1, b1, w2, b2, B, H, W, C, num_blocks, lambda, keep_fraction, dtype, out, 0};
+  return run(a, afno::kStageFull, nullptr, stream, true);
 }
 
 int afno_filter_forward_hidden(const void* x, const void* w1, const void* b1, const void* w2,

@@ -335,3 +335,26 @@ def test_stage_hidden_validation():
     # w1 of the hidden size: 4 * 16 * 32 * 8 bytes = 16 KiB, so dst 8 KiB in overlaps it
     assert call_stage_hidden(dst=W1 + 8192) == afno.AFNO_ERR_ALIAS
     assert call_stage_hidden(B=0, x=None, dst=None) == afno.AFNO_OK
+
+
+def call_noalloc(**kw):
+    a = dict(x=X, w1=W1, b1=B1, w2=W2, b2=B2, B=1, H=16, W=32, C=64, nb=4, lam=0.01, keep=1.0,
+             dtype=afno.AFNO_DTYPE_FP32, out=OUT, stream=None)
+    a.update(kw)
+    return afno.afno_filter_forward_noalloc(a["x"], a["w1"], a["b1"], a["w2"], a["b2"], a["B"],
+                                            a["H"], a["W"], a["C"], a["nb"], a["lam"], a["keep"],
+                                            a["dtype"], a["out"], a["stream"])
+
+
+def test_noalloc_validates_like_the_forward_and_bounds_its_workspace():
+    """Validation before any HIP call: the forward's checks, then the fixed workspace's bound
+    (128 MiB; the 90 x 180 x 768 bf16 filter needs B * 100.6 MB of spectrum plus 1.2 MB of
+    prepared operands, so B = 6 does not fit)."""
+    assert call_noalloc(H=0) == afno.AFNO_ERR_INVALID_ARG
+    assert call_noalloc(H=7) == afno.AFNO_ERR_UNSUPPORTED
+    assert call_noalloc(out=X) == afno.AFNO_ERR_ALIAS
+    assert call_noalloc(B=0, x=None, out=None) == afno.AFNO_OK
+    bf = dict(H=90, W=180, C=768, nb=8, dtype=afno.AFNO_DTYPE_BF16)
+    assert call_noalloc(B=6, **bf) == afno.AFNO_ERR_UNSUPPORTED
+    assert "exceeds" in afno.afno_last_error()
+    assert call_noalloc(B=50, **bf) == afno.AFNO_ERR_UNSUPPORTED
