@@ -171,7 +171,7 @@ int make_plan(const Args& a, afno::Plan& pl) {
   const size_t fb = hid ? afno::hidden_frag_bytes(pl)
                         : ((mfma || afno::use_fast_col(pl)) ? afno::frag_bytes(pl) : 0);
   pl.tab_offset = (pl.frag_offset + fb + 255) / 256 * 256;
-  pl.ws_bytes = (mfma || hid) ? pl.tab_offset + afno::mfma_tab_bytes(pl) : pl.frag_offset + fb;
+  pl.ws_bytes = (mfma || hid) ? pl.tab_offset + afno::fwd_tab_bytes(pl) : pl.frag_offset + fb;
 
   // out must not overlap any input
   const size_t xb = (size_t)a.B * a.H * a.W * a.C * es;

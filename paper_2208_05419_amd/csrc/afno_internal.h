@@ -93,6 +93,7 @@ bool use_mfma_hidden(const Plan& pl);  // matrix-core column kernel for hidden =
 size_t hidden_frag_bytes(const Plan& pl);
 size_t frag_bytes(const Plan& pl);
 size_t mfma_tab_bytes(const Plan& pl);
+size_t fwd_tab_bytes(const Plan& pl);   // the forward's tables (kept-row kernel included)
 // ev: NULL, or kProfEvents events recorded before the first kernel and after each phase
 // backward pass: modes per block of the per-mode factor tensors, and the column kernel's LDS
 int64_t bwd_mpad(const Plan& pl);

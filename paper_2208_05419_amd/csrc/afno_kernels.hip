@@ -28,6 +28,7 @@
 #include "kernels_generic.h"
 #include "kernels_mfma.h"
 #include "kernels_hidden_mfma.h"
+#include "kernels_kept_mfma.h"
 #include "kernels_backward.h"
 #include "kernels_backward_mfma.h"
 #include "kernels_block.h"
@@ -48,11 +49,11 @@ int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
 
 // tasks of the preparation job: the fragment-ordered weights' words, and the DFT table's
 // columns if with_tab
-static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h) {
+static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h, int kp = 0) {
   const int hp = mfma_col_hp(pl.H);
   return pl.nb * (pl.dtype == 0 ? frag_words_per_block<float>((int)pl.bs)
                                 : frag_words_per_block<bf16>((int)pl.bs)) +
-         (with_tab ? dft_table_tasks(hp, kept_h) : 0);
+         (with_tab ? (kp > 0 ? kept_table_tasks(hp, kp) : dft_table_tasks(hp, kept_h)) : 0);
 }
 
 #define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
@@ -77,7 +78,7 @@ static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, PrepJob<T> pj,
   if (pl.W == w) {                                                                        \
     const unsigned nmain = (unsigned)row_grid<np, (int)sizeof(T)>(gx, (int)(pl.C / (2 * np))); \
     const unsigned nprep = pj.wout ? (unsigned)(std::min<int64_t>(                        \
-        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h) + np * n1 - 1) / (np * n1), 1024) \
+        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp) + np * n1 - 1) / (np * n1), 1024) \
         + 7) / 8 * 8 : 0;                                                                 \
     pj.nprep = (int)nprep;                                                                \
     hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nprep + nmain),              \
@@ -146,12 +147,49 @@ size_t mfma_tab_bytes(const Plan& pl) {
   return (size_t)(2 * hp / 32) * (hp / 16) * 64 * 16;
 }
 
+// the kept-row column kernel (kernels_kept_mfma.h): bf16, block size 96, 64 < H <= 96, and a
+// cutoff that keeps at most 48 rows (2 kept_h - 1 <= 48); 0 elsewhere, else the padded count
+int mfma_kept_rows(const Plan& pl) {
+  if (pl.path != 0 || pl.dtype != 1 || pl.col.hs != pl.bs || pl.bs != 96 || pl.H <= 64 ||
+      pl.H > 96 || pl.kept_h < 1 || pl.kept_h > pl.H / 2)
+    return 0;
+  const int64_t nkept = 2 * pl.kept_h - 1;
+  return nkept <= 48 ? (int)((nkept + 15) / 16 * 16) : 0;
+}
+
+#define AFNO_KEPT_LIST(X) X(16) X(32) X(48)
+
+size_t kept_tab_bytes(int kp) {
+  switch (kp) {
+#define AFNO_CASE(KP_) case KP_: return (size_t)KeptCol<96, 96, KP_>::kTabBytes;
+    AFNO_KEPT_LIST(AFNO_CASE)
+#undef AFNO_CASE
+  }
+  return 0;
+}
+
+// the forward's transform tables: the kept-row kernel's where it runs, and the full table (for
+// the diagnostic spectrum stage, which needs every row)
+size_t fwd_tab_bytes(const Plan& pl) {
+  return std::max(mfma_tab_bytes(pl), kept_tab_bytes(mfma_kept_rows(pl)));
+}
+
 static void launch_col_mfma(const Plan& pl, bf16* S, const bf16* b1, const bf16* b2, int stage,
                             hipStream_t st) {
   const uint4* wf = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.frag_offset);
   const uint4* tab = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + pl.tab_offset);
   const int hp = mfma_col_hp(pl.H);
   const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
+  const int kp = stage == 1 ? 0 : mfma_kept_rows(pl);
+#define AFNO_CASE(KP_)                                                                      \
+  if (kp == KP_) {                                                                          \
+    hipLaunchKernelGGL((column_mfma_kept<96, 96, KP_>), grid, dim3(384),                   \
+                       (KeptCol<96, 96, KP_>::kBytes), st, S, wf, tab, b1, b2, (int)pl.H,   \
+                       (int)pl.C, (int)pl.KW, (int)pl.nb, (int)pl.kept_h, pl.col.lam, stage); \
+    return;                                                                                 \
+  }
+  AFNO_KEPT_LIST(AFNO_CASE)
+#undef AFNO_CASE
 #define AFNO_CASE(HP_, BS_)                                                                 \
   if (hp == HP_ && pl.bs == BS_) {                                                          \
     constexpr int lds = MfmaCol<HP_, BS_>::kBytes;                                          \
@@ -238,13 +276,14 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   // prepared column-kernel operands (after the spectrum in the workspace; independent of x):
   // extra workgroups of the size-specialised W-axis forward launch, else a launch of their own
   PrepJob<T> pj{static_cast<const T*>(w1), static_cast<const T*>(w2), nullptr, nullptr,
-                (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0, (int)pl.kept_h};
+                (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0, (int)pl.kept_h,
+                stage == kStageSpectrum ? 0 : mfma_kept_rows(pl)};
   if (col_mfma || col_fast)
     pj.wout = reinterpret_cast<typename FragWord<T>::type*>(static_cast<char*>(S) + pl.frag_offset);
   if (col_mfma) pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
   if (ev) (void)hipEventRecord(ev[0], st);
   if (pj.wout && !row_fast) {
-    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr, pj.kept_h) + 255) / 256, 4096);
+    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp) + 255) / 256, 4096);
     hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
   }
   if constexpr (sizeof(T) == 2) {
@@ -356,7 +395,7 @@ size_t bwd_acc_floats(const Plan& pl) {
 template <typename T>
 static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream_t st) {
   if (pl.path != 1 && fast_row_available(pl.W, pl.C)) {
-    PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0, -1};
+    PrepJob<T> pj{nullptr, nullptr, nullptr, nullptr, (int)pl.nb, (int)pl.bs, (int)pl.H, 0, 0, -1, 0};
     launch_row_fwd_fast<T>(pl, x, S, pj, st);
   } else {
     dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
@@ -429,8 +468,8 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
       const int64_t ntab = (int64_t)mfma_tab_bytes(pl) / 16;
       // the table rounded entry by entry (kept_h -1): tab_lo holds its remainders
       PrepJob<T> pf{static_cast<const T*>(a.w1), static_cast<const T*>(a.w2), wfwd, tab, nb, bs,
-                    (int)pl.H, hp, 0, -1};
-      PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0, -1};
+                    (int)pl.H, hp, 0, -1, 0};
+      PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0, -1, 0};
       // everything that does not read wt1 / wt2 in one launch, then their fragments
       BwdPrep bp{pf, static_cast<const bf16*>(a.w1), static_cast<const bf16*>(a.w2), wt1, wt2,
                  tab_lo, zero_from, nb, bs, (int)pl.H, hp, prep_words_host(pl, true, -1), ntab, nw,
@@ -594,6 +633,9 @@ hipError_t set_kernel_attributes() {
 #undef AFNO_CASE
 #define AFNO_CASE(HP_, BS_, HS_) AFNO_ATTR((column_mfma_hidden<HP_, BS_, HS_>))
   AFNO_MFMA_HID_LIST(AFNO_CASE)
+#undef AFNO_CASE
+#define AFNO_CASE(KP_) AFNO_ATTR((column_mfma_kept<96, 96, KP_>))
+  AFNO_KEPT_LIST(AFNO_CASE)
 #undef AFNO_CASE
 #undef AFNO_ATTR
   return first;

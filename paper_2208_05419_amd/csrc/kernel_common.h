@@ -147,6 +147,18 @@ __device__ __forceinline__ bool row_kept(int r, int H, int kept_h) {
   return s < kept_h;
 }
 
+// the rows the cutoff keeps, compacted (2 kept_h - 1 of them, kept_h <= H / 2): kept row k'
+// -> spectral row (0, 1, .., kept_h - 1, then H - kept_h + 1, .., H - 1), and back (-1: a row
+// the cutoff drops)
+__host__ __device__ __forceinline__ int kept_row(int kp, int H, int kept_h) {
+  return kp < kept_h ? kp : H - (2 * kept_h - 1 - kp);
+}
+__host__ __device__ __forceinline__ int kept_index(int h, int H, int kept_h) {
+  if (h < kept_h) return h;
+  if (h > H - kept_h) return h - (H - (2 * kept_h - 1));
+  return -1;
+}
+
 // S(v) = v - lam (v > lam), v + lam (v < -lam), else 0, written as v - clamp(v, -lam, lam)
 // (exactly 0 inside the band, exact shifts outside it)
 __device__ __forceinline__ float softshrink(float v, float lam) {

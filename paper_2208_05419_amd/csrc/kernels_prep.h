@@ -90,6 +90,60 @@ __device__ __forceinline__ void dft_table_column(int task, int H, int HP, int ke
   }
 }
 
+// The two tables of the kept-row column kernel (kernels_kept_mfma.h) for height H padded to
+// HP and KP kept rows (kept_row): the forward table Tf[(sigma, h)][k'] = T[(sigma, h)][kept_row(k')]
+// (K = 2 HP, N = KP; zero for h >= H or k' >= 2 kept_h - 1), fragment word by word with every
+// entry rounded to nearest, then the inverse table Ti[(sigma, k')][h] = T[(sigma, kept_row(k'))][h]
+// (K = 2 KP, N = HP), one column (sigma, h) per task with dft_table_column's error carry over
+// the kept rows.  Tasks: DKS KT 64 words, then 2 HP columns.  roots: dft_roots.
+__host__ __device__ inline int64_t kept_table_tasks(int HP, int KP) {
+  return (int64_t)(2 * HP / 32) * (KP / 16) * 64 + 2 * HP;
+}
+__device__ __forceinline__ void kept_table_task(int64_t i, int H, int HP, int KP, int kept_h,
+                                                const float2* roots, uint4* tout) {
+  const int KT = KP / 16, HT = HP / 16;
+  const int64_t ntf = (int64_t)(2 * HP / 32) * KT * 64;
+  const float sc = 1.0f / sqrtf((float)H);
+  const int nkept = 2 * kept_h - 1;
+  if (i < ntf) {
+    const int lane = (int)(i & 63);
+    const int f = (int)(i >> 6);
+    const int t = f % KT, s = f / KT;
+    const int kp = 16 * t + (lane & 15);
+    union { uint4 u; bf16 h[8]; } w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kap = 32 * s + 8 * (lane >> 4) + e;
+      const int sigma = kap / HP, h = kap % HP;
+      float v = 0.f;
+      if (h < H && kp < nkept) {
+        const float2 z = roots[(h * kept_row(kp, H, kept_h)) % H];
+        v = sigma == 0 ? z.x * sc : -z.y * sc;
+      }
+      w.h[e] = (bf16)v;
+    }
+    tout[i] = w.u;
+    return;
+  }
+  const int task = (int)(i - ntf);  // column (sigma, h) of Ti
+  const int sigma = task / HP, h = task - sigma * HP;
+  bf16* tb = reinterpret_cast<bf16*>(tout + ntf);
+  float err = 0.f;
+  for (int kp = 0; kp < KP; ++kp) {
+    float v = 0.f;
+    if (h < H && kp < nkept) {
+      const float2 z = roots[(kept_row(kp, H, kept_h) * h) % H];
+      v = sigma == 0 ? z.x * sc : -z.y * sc;
+    }
+    const bool carry = kp < nkept;
+    const bf16 b = (bf16)(carry ? v - err : v);
+    if (carry) err += (float)b - v;
+    const int kap = sigma * KP + kp;
+    const int64_t word = ((int64_t)(kap >> 5) * HT + (h >> 4)) * 64 + (h & 15) + 16 * ((kap >> 3) & 3);
+    tb[word * 8 + (kap & 7)] = b;
+  }
+}
+
 // What to prepare: both layers of every block in fragment order (frag_words_per_block words
 // per block, word ((layer * KSTEPS + s) * NT16 + t) * 64 + lane), then, if tout is set, the
 // DFT table for height H padded to HP: kept_h >= 0, 2 HP column tasks (dft_table_column, the
@@ -104,6 +158,7 @@ struct PrepJob {
   int nb, bs, H, HP;
   int nprep;   // workgroups the host launch gives the job (placed before its own work)
   int kept_h;  // the table's rounding, as above
+  int kp;      // > 0: the kept-row kernel's two tables for kp kept rows (kept_table_task)
 };
 
 __host__ __device__ inline int64_t dft_table_tasks(int HP, int kept_h) {
@@ -113,7 +168,8 @@ __host__ __device__ inline int64_t dft_table_tasks(int HP, int kept_h) {
 template <typename T>
 __device__ __forceinline__ int64_t prep_words(const PrepJob<T>& pj) {
   return (int64_t)pj.nb * frag_words_per_block<T>(pj.bs) +
-         (pj.tout ? dft_table_tasks(pj.HP, pj.kept_h) : 0);
+         (pj.tout ? (pj.kp > 0 ? kept_table_tasks(pj.HP, pj.kp) : dft_table_tasks(pj.HP, pj.kept_h))
+                  : 0);
 }
 
 // Tasks i, i + stride, ... of the job: one fragment word of the weights each, then the table
@@ -126,7 +182,9 @@ __device__ void prep_operands(int64_t i, int64_t stride, const PrepJob<T>& pj,
   const int64_t total = prep_words(pj);
   for (; i < total; i += stride) {
     if (i >= nw) {
-      if (pj.kept_h >= 0)
+      if (pj.kp > 0)
+        kept_table_task(i - nw, pj.H, pj.HP, pj.kp, pj.kept_h, roots, pj.tout);
+      else if (pj.kept_h >= 0)
         dft_table_column((int)(i - nw), pj.H, pj.HP, pj.kept_h, roots, pj.tout);
       else
         pj.tout[i - nw] = dft_table_word(i - nw, pj.H, pj.HP);

@@ -275,6 +275,14 @@ EDGE = [
     (1, 81, 10, 96, 1, "bf16", 0.01, 0.7),
     (2, 72, 8, 192, 2, "bf16", 0.01, 1.0),
     (1, 80, 6, 64, 2, "bf16", 0.01, 1.0),
+    # the kept-row matrix-core kernel (bf16, block size 96, 64 < H <= 96, at most 48 kept
+    # rows): 45, 27, 7 and 1 kept rows, ragged H, two blocks
+    (2, 90, 20, 192, 2, "bf16", 0.01, 0.5),
+    (1, 96, 8, 96, 1, "bf16", 0.02, 0.3),
+    (1, 81, 10, 96, 1, "bf16", 0.01, 0.1),
+    (2, 72, 40, 96, 1, "bf16", 0.01, 0.05),
+    (1, 75, 30, 96, 1, "bf16", 0.01, 0.6),
+    (1, 80, 16, 192, 2, "bf16", 0.005, 0.55),
     # H = 180 columns with the size-specialised vector-ALU transform kernels at block
     # sizes 32 (fp32 and bf16) and 64 (bf16), with and without a cutoff
     (1, 180, 24, 64, 2, "fp32", 0.01, 1.0),
