@@ -43,18 +43,20 @@ __device__ __forceinline__ int opq(int v) {
 }
 
 
-// Geometry for padded height HP (H <= HP, HP a multiple of 32) and block size BS.
-template <int HP, int BS>
+// Geometry for padded height HP (H <= HP, HP a multiple of 32) and block size BS; NWR x NWC
+// waves (transposed products: NWR along the channel entries, NWC along the rows; layer 2 the
+// other way round).
+template <int HP, int BS, int NWR = 4, int NWC = 2>
 struct MfmaCol {
-  static constexpr int kThreads = 512;
+  static constexpr int kThreads = 64 * NWR * NWC;
   static constexpr int MT = 2 * BS / 16;   // 16-entry tiles over the 2 BS channel entries
   static constexpr int KT = HP / 16;       // 16-row tiles over H (spectral or spatial rows)
   static constexpr int DKS = 2 * HP / 32;  // k-steps of a transform product (K = 2 HP)
   static constexpr int WKS = 2 * BS / 32;  // k-steps of an MLP product (K = 2 BS)
-  // products with channel-entry rows and field-row columns: 4 x 2 waves
-  static constexpr int TWM = 4, TWN = 2, TMW = MT / TWM, TNW = KT / TWN;
-  // layer 2 (field-row rows, channel-entry columns): 2 x 4 waves
-  static constexpr int LWM = 2, LWN = 4, LMW = KT / LWM, LNW = MT / LWN;
+  // products with channel-entry rows and field-row columns: NWR x NWC waves
+  static constexpr int TWM = NWR, TWN = NWC, TMW = MT / TWM, TNW = KT / TWN;
+  // layer 2 (field-row rows, channel-entry columns): NWC x NWR waves
+  static constexpr int LWM = NWC, LWN = NWR, LMW = KT / LWM, LNW = MT / LWN;
   static_assert(HP % 32 == 0 && BS % 32 == 0, "HP and BS multiples of 32");
   static_assert(MT % TWM == 0 && KT % TWN == 0 && KT % LWM == 0 && MT % LWN == 0, "wave grid");
   static constexpr int kTabWords = DKS * KT * 64;  // 16-byte table fragments
@@ -95,11 +97,9 @@ __device__ __forceinline__ f32x4 mma_bf16(uint4 a, uint4 b, f32x4 c) {
 // A transform product over the planar planes P (X for the forward, O for the inverse):
 // acc[m][n] += A (channel-entry tile TMW wm + m) x T (row tile TNW wn + n), the A operand
 // taking plane rho ^ sigma, negated where rho == neg_rho on the sigma = 1 planes.
-template <int HP, int BS>
+template <int HP, int BS, class G = MfmaCol<HP, BS>>
 __device__ __forceinline__ void dft_product(const bf16* P, const uint4* tab, int lane, int wm,
-                                            int wn, int neg_rho,
-                                            f32x4 (&acc)[MfmaCol<HP, BS>::TMW][MfmaCol<HP, BS>::TNW]) {
-  typedef MfmaCol<HP, BS> G;
+                                            int wn, int neg_rho, f32x4 (&acc)[G::TMW][G::TNW]) {
   const int l16 = lane & 15, g = lane >> 4, rho = l16 & 1;
   const uint32_t neg = rho == neg_rho ? 0x80008000u : 0u;
   const bf16* pl0 = P + rho * G::kPlane + 8 * g;          // plane rho (sigma = 0)
@@ -134,12 +134,12 @@ __device__ __forceinline__ void dft_product(const bf16* P, const uint4* tab, int
 // S: spectrum [B][H][KW][C] complex bf16, updated in place.  wfrag: fragment-ordered
 // weights; dtab: transform table (both from prep_operands).  stage: 0 full, 1 stop after the
 // forward transform, 2 stop after the MLP (the column goes back to S as it is).
-template <int HP, int BS>
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
+template <int HP, int BS, int NWR = 4, int NWC = 2>
+__global__ void __launch_bounds__(64 * NWR * NWC) __attribute__((amdgpu_waves_per_eu(NWR * NWC / 2)))
 column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* __restrict__ dtab,
             const bf16* __restrict__ b1, const bf16* __restrict__ b2, int H, int C, int KW,
             int nb, int kept_h, float lam, int stage) {
-  typedef MfmaCol<HP, BS> G;
+  typedef MfmaCol<HP, BS, NWR, NWC> G;
   extern __shared__ uint4 smem_mfma[];
   uint4* tab = smem_mfma;
   bf16* R = reinterpret_cast<bf16*>(reinterpret_cast<char*>(smem_mfma) + G::kTabBytes);
@@ -218,7 +218,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
   {
     const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
-    dft_product<HP, BS>(R, tab, lane, twm, twn, 0, acc);
+    dft_product<HP, BS, G>(R, tab, lane, twm, twn, 0, acc);
     __syncthreads();  // every wave has read its X fragments
 #pragma unroll
     for (int m = 0; m < G::TMW; ++m)
@@ -370,7 +370,7 @@ column_mfma(bf16* __restrict__ S, const uint4* __restrict__ wfrag, const uint4* 
   {
     const int lane = opq((int)threadIdx.x) & 63, l16 = lane & 15, g = lane >> 4;
     f32x4 acc[G::TMW][G::TNW];
-    dft_product<HP, BS>(R, tab, lane, twm, twn, 1, acc);
+    dft_product<HP, BS, G>(R, tab, lane, twm, twn, 1, acc);
     __syncthreads();  // every wave has read its O fragments
 #pragma unroll
     for (int m = 0; m < G::TMW; ++m)
