@@ -46,6 +46,13 @@ PREWARM_S = 0.3                # untimed sustained run before the counted warm-u
 # with 192 hidden units per block of 96 (hidden-size factor 2)
 OTHER_WORKLOADS = ("afno90x180_c768_nb8_fp32", "afno180x360_c1024_nb8_bf16",
                    "afno180x360_c1024_nb32_bf16", "afno90x180_c768_nb8_hs192_bf16_b4")
+# the five workloads whose oracle time per sample the CPU baseline reports
+CPU_CONFIGS = ("afno16x32_c64_nb4_fp32", "afno90x180_c768_nb8_fp32", "afno90x180_c768_nb8_bf16_b4",
+               "afno180x360_c1024_nb8_bf16", "afno90x180_c768_nb8_bf16_ens100_keep0.5")
+# how the column kernel evaluates the H-axis DFTs of the headline workload: matrix-core
+# products (bf16 operands, fp32 accumulation) against a DFT table whose entries are rounded to
+# bf16 with the rounding error carried down each column
+H_TRANSFORM = "matrix-core DFT, bf16 table with error-carrying rounding, fp32 accumulation"
 # HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
 # sha256 of the kernel sources it was measured on (null once the kernels change)
 
@@ -281,26 +288,49 @@ def roofline(wl, kern_ms: dict, es: int):
 
 def cpu_baseline(wl, min_seconds: float):
     """The float64 oracle on the workload's samples, one sample per call, repeated until
-    at least min_seconds of wall time have passed."""
+    at least min_seconds of wall time have passed; then one sample of each of the other four
+    workloads alone (per_config: wall seconds per sample and samples/s)."""
     import oracle
     from paper_2208_05419_amd import synth
 
-    x = synth.widen(synth.make_x(wl), wl.dtype)
-    w = {k: synth.widen(v, wl.dtype) for k, v in synth.make_weights(wl).items()}
+    def one(w_, x_, b):
+        oracle.filter_forward(x_[b:b + 1], w_["w1"], w_["b1"], w_["w2"], w_["b2"],
+                              w_["nb"], w_["lam"], w_["keep"])
+
+    def inputs(wl_, members=None):
+        x_ = synth.widen(synth.make_x(wl_, members=members), wl_.dtype)
+        w_ = {k: synth.widen(v, wl_.dtype) for k, v in synth.make_weights(wl_).items()}
+        w_.update(nb=wl_.num_blocks, lam=wl_.lam, keep=wl_.keep)
+        return x_, w_
+
+    x, w = inputs(wl)
     done = 0
     t0 = time.perf_counter()
     while True:
-        b = done % wl.B
-        oracle.filter_forward(x[b:b + 1], w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks,
-                              wl.lam, wl.keep)
+        one(w, x, done % wl.B)
         done += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
             break
+    per_config = {wl.name: {"sample_s": round(dt / done, 4), "samples_per_s": round(done / dt, 4),
+                            "timed": f"{done} samples"}}
+    for name in CPU_CONFIGS:
+        if name == wl.name:
+            continue
+        c = synth.WORKLOADS[name]
+        xc, wc = inputs(c, members=[0] if c.x_kind == "ensemble" else None)
+        note = "sample 0" if c.x_kind != "ensemble" else "member 0"
+        t1 = time.perf_counter()
+        one(wc, xc, 0)
+        s = time.perf_counter() - t1
+        per_config[name] = {"sample_s": round(s, 4), "samples_per_s": round(1.0 / s, 4),
+                            "timed": note}
     return {"value": round(done / dt, 4), "unit": "samples/s", "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"{done} single-sample calls cycling over the {wl.B} samples of {wl.name} "
-                      f"(float64 direct DFT, {dt:.1f} s wall)"}
+                      f"(float64 direct DFT, {dt:.1f} s wall); per_config: the oracle's time per sample "
+                      f"of each of the five workloads",
+            "per_config": per_config}
 
 
 def calibration_copy(mib: int):
@@ -376,7 +406,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C,
-                   "num_blocks": wl.num_blocks, "lambda": wl.lam, "keep_fraction": wl.keep},
+                   "num_blocks": wl.num_blocks, "lambda": wl.lam, "keep_fraction": wl.keep,
+                   "h_transform": H_TRANSFORM},
         "roofline": roof,
         "kernels": per_kernel,
         "timed_calls": calls,
@@ -400,7 +431,7 @@ def main():
         for name in OTHER_WORKLOADS:
             o = synth.WORKLOADS[name]
             o_es = 2 if o.dtype == "bf16" else 4
-            o_ms, o_kern, _, _ = time_workload(o, max(args.steps // 5, 10), max(args.warmup // 5, 3))
+            o_ms, o_kern, _, _ = time_workload(o, max(args.steps, 100), max(args.warmup // 5, 3))
             _, o_per = roofline(o, o_kern, o_es)
             others[name] = {"samples_per_s": round(o.B / (o_ms * 1e-3), 2), "ms_per_step": round(o_ms, 4),
                             "kernel_ms": {k: v["ms"] for k, v in o_per.items()}}
