@@ -126,12 +126,12 @@ static void launch_col_fast(const Plan& pl, T* S, const T* b1, const T* b2, int 
   else if (pl.H == 90 && pl.bs == 96)
     launch_col_fast_one<T, float, 90, 9, 10, 96, 4, 512>(pl, S, wf, b1, b2, stage, st);
   else if (pl.H == 180 && pl.bs == 32)
-    launch_col_fast_one<T, float, 180, 12, 15, 32, 3, 256>(pl, S, wf, b1, b2, stage, st);
+    launch_col_fast_one<T, float, 180, 12, 15, 32, 6, 512>(pl, S, wf, b1, b2, stage, st);
   else if constexpr (sizeof(T) == 2) {
     if (pl.bs == 64)
       launch_col_fast_one<T, bf16, 180, 12, 15, 64, 3, 256>(pl, S, wf, b1, b2, stage, st);
     else
-      launch_col_fast_one<T, bf16, 180, 12, 15, 128, 2>(pl, S, wf, b1, b2, stage, st);
+      launch_col_fast_one<T, bf16, 180, 12, 15, 128, 4, 1024>(pl, S, wf, b1, b2, stage, st);
   }
 }
 
@@ -624,9 +624,9 @@ hipError_t set_kernel_attributes() {
 #undef AFNO_CASE
   AFNO_ATTR((column_fast<float, float, 90, 9, 10, 96, 4, 512>))
   AFNO_ATTR((column_fast<bf16, float, 90, 9, 10, 96, 4, 512>))
-  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 2, 512>))
-  AFNO_ATTR((column_fast<float, float, 180, 12, 15, 32, 3, 256>))
-  AFNO_ATTR((column_fast<bf16, float, 180, 12, 15, 32, 3, 256>))
+  AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 128, 4, 1024>))
+  AFNO_ATTR((column_fast<float, float, 180, 12, 15, 32, 6, 512>))
+  AFNO_ATTR((column_fast<bf16, float, 180, 12, 15, 32, 6, 512>))
   AFNO_ATTR((column_fast<bf16, bf16, 180, 12, 15, 64, 3, 256>))
 #define AFNO_CASE(HP_, BS_) AFNO_ATTR((column_mfma<HP_, BS_>))
   AFNO_MFMA_COL_LIST(AFNO_CASE)

@@ -40,14 +40,18 @@ __device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, con
   const int64_t l1 = (int64_t)(2 * bs / 32) * mh * 64;
   const int64_t per_block = 2 * l1;
   const int64_t nw = (int64_t)nb * per_block;
-  const int64_t total = nw + (tout ? (int64_t)2 * HP : 0);
+  // the table's column tasks first: each is a sequential pass over a column, so they start
+  // in the launch's first workgroup
+  const int64_t ntab = tout ? (int64_t)2 * HP : 0;
+  const int64_t total = nw + ntab;
   for (; i < total; i += stride) {
-    if (i >= nw) {
-      dft_table_column((int)(i - nw), H, HP, kept_h, roots, tout);
+    if (i < ntab) {
+      dft_table_column((int)i, H, HP, kept_h, roots, tout);
       continue;
     }
-    const int64_t blk = i / per_block;
-    int64_t u = i - blk * per_block;
+    const int64_t q = i - ntab;  // weight word q
+    const int64_t blk = q / per_block;
+    int64_t u = q - blk * per_block;
     const int layer = u >= l1 ? 1 : 0;
     u -= layer * l1;
     const int lane = (int)(u & 63);
@@ -57,7 +61,7 @@ __device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, con
     const bf16* w = layer ? w2 + blk * (int64_t)hs * bs * 2 : w1 + blk * (int64_t)bs * hs * 2;
     const int n_out = layer ? bs : hs;
     const int j = (16 * t + (lane & 15)) >> 1;
-    wout[i] = FragWord<bf16>::make(w, n_out, s * 32, j, lane & 1, lane);
+    wout[q] = FragWord<bf16>::make(w, n_out, s * 32, j, lane & 1, lane);
   }
 }
 

@@ -46,8 +46,8 @@ __device__ __forceinline__ void dft_roots(float2* roots, int H) {
   __syncthreads();
 }
 
-// One column (sigma, j) of the transform table: T[(sigma, r)][j] for every r < HP, each entry
-// stored at its place in dft_table_word's fragment order (2-byte stores), from the roots of
+// One column (sigma, j) of the transform table: T[(sigma, r)][j] for every r < HP, stored as
+// the HP / 8 fragment words of dft_table_word's order that hold it, from the roots of
 // dft_roots.  The matrix-core column kernels apply this one table in both directions, and the
 // inverse's sum over the kept rows k of T[(sigma, k)][h] O[k] meets a component of O that is
 // the same at every kept row (the biases put one there, tens of times the rest): with each
@@ -61,10 +61,11 @@ __device__ __forceinline__ void dft_table_column(int task, int H, int HP, int ke
                                                  const float2* roots, uint4* tout) {
   const int sigma = task / HP, j = task - sigma * HP;
   const int KT = HP / 16;
-  bf16* tb = reinterpret_cast<bf16*>(tout);
   const float sc = 1.0f / sqrtf((float)H);
   const bool all_rows = kept_h > H / 2;
+  const int jm = j < H ? j : 0;
   float err = 0.f;
+  int m = 0;  // (r j) mod H, stepped
   for (int r0 = 0; r0 < HP; r0 += 8) {
     float v[8];
 #pragma unroll
@@ -72,21 +73,24 @@ __device__ __forceinline__ void dft_table_column(int task, int H, int HP, int ke
       const int r = r0 + e;
       v[e] = 0.f;
       if (r < H && j < H) {
-        const float2 z = roots[(r * j) % H];
+        const float2 z = roots[m];
         v[e] = sigma == 0 ? z.x * sc : -z.y * sc;
       }
+      m += jm;
+      m = m >= H ? m - H : m;
     }
+    union { uint4 u; bf16 h[8]; } w;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int r = r0 + e;
       const bool carry = r < H && (all_rows || row_kept(r, H, kept_h));
       const bf16 b = (bf16)(carry ? v[e] - err : v[e]);
       if (carry) err += (float)b - v[e];
-      const int kap = sigma * HP + r;  // K row of the real-ified table
-      const int64_t word =
-          ((int64_t)(kap >> 5) * KT + (j >> 4)) * 64 + (j & 15) + 16 * ((kap >> 3) & 3);
-      tb[word * 8 + (kap & 7)] = b;
+      w.h[e] = b;
     }
+    // the 8 entries of K rows sigma HP + r0 .. + 7 make one fragment word of column j
+    const int kap = sigma * HP + r0;
+    tout[((int64_t)(kap >> 5) * KT + (j >> 4)) * 64 + (j & 15) + 16 * ((kap >> 3) & 3)] = w.u;
   }
 }
 
@@ -127,20 +131,25 @@ __device__ __forceinline__ void kept_table_task(int64_t i, int H, int HP, int KP
   }
   const int task = (int)(i - ntf);  // column (sigma, h) of Ti
   const int sigma = task / HP, h = task - sigma * HP;
-  bf16* tb = reinterpret_cast<bf16*>(tout + ntf);
+  uint4* ti = tout + ntf;
   float err = 0.f;
-  for (int kp = 0; kp < KP; ++kp) {
-    float v = 0.f;
-    if (h < H && kp < nkept) {
-      const float2 z = roots[(kept_row(kp, H, kept_h) * h) % H];
-      v = sigma == 0 ? z.x * sc : -z.y * sc;
+  for (int kp0 = 0; kp0 < KP; kp0 += 8) {
+    union { uint4 u; bf16 h[8]; } w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kp = kp0 + e;
+      float v = 0.f;
+      if (h < H && kp < nkept) {
+        const float2 z = roots[(kept_row(kp, H, kept_h) * h) % H];
+        v = sigma == 0 ? z.x * sc : -z.y * sc;
+      }
+      const bool carry = kp < nkept;
+      const bf16 b = (bf16)(carry ? v - err : v);
+      if (carry) err += (float)b - v;
+      w.h[e] = b;
     }
-    const bool carry = kp < nkept;
-    const bf16 b = (bf16)(carry ? v - err : v);
-    if (carry) err += (float)b - v;
-    const int kap = sigma * KP + kp;
-    const int64_t word = ((int64_t)(kap >> 5) * HT + (h >> 4)) * 64 + (h & 15) + 16 * ((kap >> 3) & 3);
-    tb[word * 8 + (kap & 7)] = b;
+    const int kap = sigma * KP + kp0;  // 8 K rows: one fragment word of column h
+    ti[((int64_t)(kap >> 5) * HT + (h >> 4)) * 64 + (h & 15) + 16 * ((kap >> 3) & 3)] = w.u;
   }
 }
 
