@@ -53,6 +53,7 @@ CPU_CONFIGS = ("afno16x32_c64_nb4_fp32", "afno90x180_c768_nb8_fp32", "afno90x180
 # products (bf16 operands, fp32 accumulation) against a DFT table whose entries are rounded to
 # bf16 with the rounding error carried down each column
 H_TRANSFORM = "matrix-core DFT, bf16 table with error-carrying rounding, fp32 accumulation"
+H_TRANSFORM_VALU = "vector-ALU FFT, fp32 arithmetic (bf16 storage between passes)"
 # HBM traffic measured with rocprofv3 FETCH_SIZE / WRITE_SIZE, per launch, keyed by the
 # sha256 of the kernel sources it was measured on (null once the kernels change)
 
@@ -413,6 +414,18 @@ def main():
         "timed_calls": calls,
         "call_ms": dist,
     }
+    if not args.no_others:
+        # the same workload with the H transforms as vector-ALU FFTs in fp32 arithmetic (the
+        # precision of the paper's own FFTs), for comparison with the matrix-core table
+        afno.set_kernel_path(afno.AFNO_PATH_VALU_DFT)
+        try:
+            v_ms, v_kern, _, _ = time_workload(wl, args.steps, max(args.warmup // 2, 3))
+        finally:
+            afno.set_kernel_path(afno.AFNO_PATH_AUTO)
+        _, v_per = roofline(wl, v_kern, es)
+        line["h_transform_valu_fft"] = {
+            "h_transform": H_TRANSFORM_VALU, "samples_per_s": round(wl.B / (v_ms * 1e-3), 2),
+            "ms_per_step": round(v_ms, 5), "kernel_ms": {k: v["ms"] for k, v in v_per.items()}}
     if not args.no_backward:
         line["backward"] = time_backward(wl, max(args.steps // 2, 10), max(args.warmup // 2, 3))
     if not args.no_block:

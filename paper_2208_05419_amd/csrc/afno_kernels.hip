@@ -370,14 +370,15 @@ size_t bwd_prep_bytes(const Plan& pl) {
 }
 
 // chunks of the slab weight-gradient kernel (bf16, 2 bs = 64, 128 or 192), 0 where the
-// tiled kernel runs instead; *kchunk: modes per chunk (a multiple of 32).  About two
-// workgroups per compute unit.
+// tiled kernel runs instead; *kchunk: modes per chunk (a multiple of 64).  About one
+// workgroup per compute unit; a chunk's byte offsets stay 32-bit.
 int wgrad_slab_chunks(const Plan& pl, int* kchunk) {
   const int64_t nb2 = 2 * pl.bs;
   if (pl.dtype != 1 || (nb2 != 64 && nb2 != 128 && nb2 != 192)) return 0;
   const int64_t mpad = bwd_mpad(pl);
-  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(64, 512 / (2 * pl.nb)));
-  const int64_t kc = std::max<int64_t>(32, ((mpad + want - 1) / want + 31) / 32 * 32);
+  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(64, 256 / (2 * pl.nb)));
+  const int64_t kc = std::max<int64_t>(64, ((mpad + want - 1) / want + 63) / 64 * 64);
+  if ((kc / 8 + 3 * 8) * nb2 * 16 > (int64_t)0xffffffffll) return 0;
   *kchunk = (int)kc;
   return (int)((mpad + kc - 1) / kc);
 }
@@ -497,13 +498,13 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   if (nslab > 0) {
     const dim3 sgrid((unsigned)(2 * nb * nslab));
     if (nb2 == 64)
-      hipLaunchKernelGGL(wgrad_slab<64>, sgrid, dim3(512), 256 * 64, st,
+      hipLaunchKernelGGL(wgrad_slab<64>, sgrid, dim3(1024), 512 * 64, st,
                          reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
     else if (nb2 == 128)
-      hipLaunchKernelGGL(wgrad_slab<128>, sgrid, dim3(512), 256 * 128, st,
+      hipLaunchKernelGGL(wgrad_slab<128>, sgrid, dim3(1024), 512 * 128, st,
                          reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
     else
-      hipLaunchKernelGGL(wgrad_slab<192>, sgrid, dim3(512), 256 * 192, st,
+      hipLaunchKernelGGL(wgrad_slab<192>, sgrid, dim3(1024), 512 * 192, st,
                          reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
     hipLaunchKernelGGL(wgrad_finalize_parts, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
                        dim3(256), 0, st, acc, nslab, dbias, nb, bs, a.dw1, a.dw2, a.db1, a.db2);

@@ -432,91 +432,115 @@ __global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ 
 
 // bf16 weight-gradient products for 2 bs = NB2 a multiple of 64: one workgroup per (layer,
 // block, mode chunk) computes the chunk's whole NB2 x NB2 product, so each per-mode operand is
-// read from HBM once.  Per 32-mode k-step the two operand slabs (4 mode groups x NB2 entries x
-// 16 bytes each) stream through LDS, double buffered, the next step's global loads in flight
-// during the current step's products; 8 waves as 4 x 2, each (NB2 / 64) x (NB2 / 32) output
-// tiles of 16 x 16.  The chunk's sums go to part[chunk][layer][blk][r][s] (plain stores).
-// grid 2 nb nchunk (layer, block, chunk with block fastest), 512 threads, dynamic LDS
-// 4 * 4 * NB2 * 16 bytes.
+// read from HBM once.  Per 64-mode step the two operand slabs (8 mode groups x NB2 entries x
+// 16 bytes each) stream through LDS, double buffered; the global loads of the two following
+// steps are in flight (in registers) during the current step's products, so that a workgroup
+// keeps two steps' bytes on the way from HBM.  16 waves as 4 x 4, each (NB2 / 64)^2 output
+// tiles of 16 x 16 (one workgroup per compute unit).  Words beyond the chunk's modes read 0
+// (buffer range check).  The chunk's sums go to part[chunk][layer][blk][r][s] (plain stores).
+// grid 2 nb nchunk (layer, block, chunk with block fastest), 1024 threads, dynamic LDS
+// 2 * 2 * 8 * NB2 * 16 bytes; kchunk a multiple of 64.
 template <int NB2>
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
-wgrad_slab(const bf16* __restrict__ modes, int64_t mpad,
-                                                  int nb, int kchunk, float* __restrict__ part) {
-  constexpr int RT = NB2 / 64, CT = NB2 / 32;
-  constexpr int SLAB = 4 * NB2;                   // 16-byte words per operand and k-step
-  constexpr int LW = 2 * SLAB / 512;              // words each thread moves per k-step
-  static_assert(2 * SLAB % 512 == 0, "whole words per thread");
-  extern __shared__ uint4 slab_lds[];             // [2 buffers][2 operands][SLAB]
+__global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ modes, int64_t mpad,
+                                                   int nb, int kchunk, float* __restrict__ part) {
+  constexpr int T = NB2 / 64;       // output tiles per wave along each axis
+  constexpr int SLAB = 8 * NB2;     // 16-byte words per operand and step
+  constexpr int LW = 2 * SLAB / 1024;  // words each thread moves per step
+  static_assert(SLAB % 64 == 0 && 2 * SLAB % 1024 == 0, "operand uniform per wave, whole words");
+  extern __shared__ uint4 slab_lds[];  // [2 buffers][2 operands][SLAB]
   const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, gq = lane >> 4;
-  const int wave = tid >> 6, wr = wave >> 1, wc = wave & 1;
+  const int wave = tid >> 6, wr = wave >> 2, wc = wave & 3;
   int g = blockIdx.x;
   const int blk = g % nb;
   g /= nb;
   const int layer = g & 1;
   const int chunk = g >> 1;
-  const uint4* A = reinterpret_cast<const uint4*>(
-      modes + ((int64_t)(layer ? kModeH : kModeX) * nb + blk) * NB2 * mpad);
-  const uint4* Bm = reinterpret_cast<const uint4*>(
-      modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * NB2 * mpad);
   const int64_t k0 = (int64_t)chunk * kchunk;
   const int64_t k1 = k0 + kchunk < mpad ? k0 + kchunk : mpad;
-  const int steps = (int)((k1 - k0) / 32);
-
-  // word w of a k-step: operand w / SLAB, mode group (w % SLAB) / NB2, entry w % NB2
-  const uint4* src[LW];
-  int64_t soff[LW];
+  const int steps = (int)((k1 - k0 + 63) / 64);
+  // the chunk's words of each operand: groups k0 / 8 .. k1 / 8, NB2 words each
+  const uint32_t cbytes = buf_bytes((uint64_t)(k1 - k0) / 8 * NB2 * 16);
+  const int64_t cw = (k0 >> 3) * NB2;
+  const Buf ra(reinterpret_cast<const uint4*>(
+                   modes + ((int64_t)(layer ? kModeH : kModeX) * nb + blk) * NB2 * mpad) + cw,
+               cbytes);
+  const Buf rb(reinterpret_cast<const uint4*>(
+                   modes + ((int64_t)(layer ? kModeDo : kModeDv) * nb + blk) * NB2 * mpad) + cw,
+               cbytes);
+  // word w = tid + 1024 i of a step: operand w / SLAB (uniform per wave), word w % SLAB of
+  // that operand's slab, which starts 8 NB2 words further on each step
+  uint32_t voff[LW];
+  bool opb[LW];
 #pragma unroll
   for (int i = 0; i < LW; ++i) {
-    const int w = tid + 512 * i;
-    const int op = w / SLAB, idx = w - op * SLAB;
-    const int q = idx / NB2, r = idx - q * NB2;
-    src[i] = op ? Bm : A;
-    soff[i] = (k0 >> 3) * NB2 + q * NB2 + r;
+    const int w = tid + 1024 * i;
+    opb[i] = __builtin_amdgcn_readfirstlane(w / SLAB) != 0;
+    voff[i] = (uint32_t)(w % SLAB) * 16u;
   }
-  f32x4 acc[RT][CT];
+  auto load = [&](uint4 (&r)[LW], int s) {
+    // the step's offset goes into the per-lane offset, which the range check covers
+    const uint32_t so = (uint32_t)s * (uint32_t)(SLAB * 16);
 #pragma unroll
-  for (int i = 0; i < RT; ++i)
+    for (int i = 0; i < LW; ++i) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(opb[i] ? rb.r : ra.r, voff[i] + so, 0, 0);
+      r[i] = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+  };
+  auto stash = [&](const uint4 (&r)[LW], int buf) {
 #pragma unroll
-    for (int j = 0; j < CT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < LW; ++i) slab_lds[buf * 2 * SLAB + tid + 1024 * i] = r[i];
+  };
+  f32x4 acc[T][T];
+#pragma unroll
+  for (int i = 0; i < T; ++i)
+#pragma unroll
+    for (int j = 0; j < T; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const uint4* LA = slab_lds + buf * 2 * SLAB + (4 * kk + gq) * NB2 + l16;
+      const uint4* LB = LA + SLAB;
+      uint4 a[T], b[T];
+#pragma unroll
+      for (int i = 0; i < T; ++i) a[i] = LA[16 * (wr * T + i)];
+#pragma unroll
+      for (int j = 0; j < T; ++j) b[j] = LB[16 * (wc * T + j)];
+#pragma unroll
+      for (int i = 0; i < T; ++i)
+#pragma unroll
+        for (int j = 0; j < T; ++j) acc[i][j] = mma_bf16(a[i], b[j], acc[i][j]);
+    }
+  };
   if (steps > 0) {
-    uint4 rv[LW];
-#pragma unroll
-    for (int i = 0; i < LW; ++i) rv[i] = src[i][soff[i]];
-#pragma unroll
-    for (int i = 0; i < LW; ++i) slab_lds[tid + 512 * i] = rv[i];
-  }
-  __syncthreads();
-  for (int s = 0; s < steps; ++s) {
-    const int buf = s & 1;
-    // the next k-step's words (4 mode groups further on; the last step reloads its own, so
-    // that loads and stores stay unconditional and the words stay in registers)
-    const int64_t nxt = (int64_t)(s + 1 < steps ? s + 1 : s) * 4 * NB2;
-    uint4 nv[LW];
-#pragma unroll
-    for (int i = 0; i < LW; ++i) nv[i] = src[i][soff[i] + nxt];
-    const uint4* LA = slab_lds + buf * 2 * SLAB + gq * NB2 + l16;
-    const uint4* LB = LA + SLAB;
-    uint4 a[RT], b[CT];
-#pragma unroll
-    for (int i = 0; i < RT; ++i) a[i] = LA[16 * (wr * RT + i)];
-#pragma unroll
-    for (int j = 0; j < CT; ++j) b[j] = LB[16 * (wc * CT + j)];
-#pragma unroll
-    for (int i = 0; i < RT; ++i)
-#pragma unroll
-      for (int j = 0; j < CT; ++j) acc[i][j] = mma_bf16(a[i], b[j], acc[i][j]);
-#pragma unroll
-    for (int i = 0; i < LW; ++i) slab_lds[(buf ^ 1) * 2 * SLAB + tid + 512 * i] = nv[i];
+    // two register sets take turns, so that no step's words are copied between registers;
+    // the steps run in pairs (a step past the chunk reads zeros and adds nothing).  The
+    // scheduling barriers keep each step's loads issued before the products they overlap.
+    uint4 r0[LW], r1[LW];
+    load(r0, 0);
+    load(r1, 1);
+    stash(r0, 0);
     __syncthreads();
+    for (int s = 0; s < steps; s += 2) {
+      load(r0, s + 2);  // buffer 0 was read last in step s
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      stash(r1, 1);
+      __syncthreads();
+      load(r1, s + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      stash(r0, 0);
+      __syncthreads();
+    }
   }
   float* out = part + (((int64_t)chunk * 2 + layer) * nb + blk) * NB2 * NB2;
 #pragma unroll
-  for (int i = 0; i < RT; ++i)
+  for (int i = 0; i < T; ++i)
 #pragma unroll
-    for (int j = 0; j < CT; ++j) {
-      const int col = 16 * (wc * CT + j) + l16;
+    for (int j = 0; j < T; ++j) {
+      const int col = 16 * (wc * T + j) + l16;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) out[(16 * (wr * RT + i) + 4 * gq + q) * NB2 + col] = acc[i][j][q];
+      for (int q = 0; q < 4; ++q) out[(16 * (wr * T + i) + 4 * gq + q) * NB2 + col] = acc[i][j][q];
     }
 }
 
