@@ -582,7 +582,10 @@ hipError_t launch_block(const Plan& pl, const BlockPtrs& a, hipStream_t st) {
   auto gemm = [&](auto epi, const bf16* Am, const bf16* Bm, const bf16* bias, const bf16* Rm,
                   bf16* Dm, int N, int K) {
     constexpr int E = decltype(epi)::value;
-    if (N % 256 == 0)
+    if (N % 256 == 0 && K % 128 == 0)
+      hipLaunchKernelGGL((gemm_dma<E>), dim3((unsigned)(mbp * (N / 256))), dim3(1024), 0, st, Am,
+                         Bm, bias, Rm, Dm, (int)M, N, K);
+    else if (N % 256 == 0)
       hipLaunchKernelGGL((gemm_bf16<E, 256>), dim3((unsigned)(mbp * (N / 256))),
                          dim3(GemmGeo<256>::NT), GemmGeo<256>::kBytes, st, Am, Bm, bias, Rm, Dm,
                          (int)M, N, K);

@@ -308,4 +308,149 @@ __global__ void __launch_bounds__(GemmGeo<BN>::NT) gemm_bf16(const bf16* __restr
   }
 }
 
+// The same product with the k-stages moved by the direct-to-LDS loads (global_load_lds_dwordx4:
+// each lane's 16 bytes go straight into the LDS, no registers or LDS store instructions in
+// between), so that three stages can be in flight during the current one's products.
+// Workgroup tile 256 x 256, 32-deep k-stages in a ring of four LDS stages (A slab 256 x 32,
+// then B slab 256 x 32, 32 KB each), 16 waves as 4 x 4 of 64 x 64.  Slab rows are 64 bytes
+// (four 16-byte chunks) without padding; chunk c of row r sits at position c ^ 2((r / 8) % 2),
+// so that the 32 lanes of each ds_read_b128 pass (rows 0-15, two chunks each) cover the 64
+// banks once.  A wave's load moves 16 consecutive rows (lane i: row i / 4, position i % 4).
+// The four stages are separate arrays: the compiler then sees that a stage being read is not
+// one whose loads are still in flight, and the loop waits on exactly the current stage's loads
+// (per wave: two loads per stage, in issue order).  The loads of the last stages' successors
+// re-read the last stage into a buffer nobody reads, so every wait counts the same.  Epilogue
+// as gemm_bf16's, 64 rows at a time, each 16-row tile row staged in its own array.
+// N a multiple of 256, K a multiple of 128; grid 8 ceil(MB / 8) (N / 256), 1024 threads, no
+// dynamic LDS.
+__shared__ uint4 gd_stage0[2048];
+__shared__ uint4 gd_stage1[2048];
+__shared__ uint4 gd_stage2[2048];
+__shared__ uint4 gd_stage3[2048];
+
+template <int EPI>
+__global__ void __launch_bounds__(1024) gemm_dma(const bf16* __restrict__ A,
+                                                 const bf16* __restrict__ Bt,
+                                                 const bf16* __restrict__ bias,
+                                                 const bf16* __restrict__ R,
+                                                 bf16* __restrict__ D, int M, int N, int K) {
+  constexpr int BM = 256, BN = 256, BK = 32, LDC = BN + 4;
+  const int nbn = N / BN;
+  const int g = blockIdx.x, xcd = g & 7, i = g >> 3;
+  const int mb = (i / nbn) * 8 + xcd, nbk = i - (i / nbn) * nbn;
+  const int m0 = mb * BM, n0 = nbk * BN;
+  if (m0 >= M) return;  // padding workgroups: the whole group leaves before any barrier
+
+  const int tid = threadIdx.x, lane = tid & 63, l16 = lane & 15, gq = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), wm = wave >> 2, wn = wave & 3;
+  const int S = K / BK;
+  // this lane's load: row 16 wave + lane / 4 of both slabs, chunk (lane % 4) ^ swizzle
+  const int lr = lane >> 2, lc = (lane & 3) ^ (2 * ((lr >> 3) & 1));
+  const bf16* ga = A + (int64_t)min(m0 + 16 * wave + lr, M - 1) * K + 8 * lc;
+  const bf16* gb = Bt + (int64_t)(n0 + 16 * wave + lr) * K + 8 * lc;
+  // this lane's operand slot in a 16-row group: row l16, chunk gq
+  const int fs = 4 * l16 + (gq ^ (2 * ((l16 >> 3) & 1)));
+
+  auto issue = [&](uint4* st, int s) {
+    const int64_t kk = (int64_t)(s < S ? s : S - 1) * BK;
+    __builtin_amdgcn_global_load_lds(ga + kk, st + 64 * wave, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(gb + kk, st + 1024 + 64 * wave, 16, 0, 0);
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const uint4* st) {
+    uint4 fa[4], fb[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) fa[a] = st[(4 * wm + a) * 64 + fs];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) fb[b] = st[1024 + (4 * wn + b) * 64 + fs];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = mma_bf16(fa[a], fb[b], acc[a][b]);
+  };
+  // this wave's loads of the current stage done (the two later stages' four loads may still
+  // be in flight), then every wave's: the barrier also tells that the stage read last is free
+  auto sync = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0x0f74);  // vmcnt(4), no wait on the other counters
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  issue(gd_stage0, 0);
+  issue(gd_stage1, 1);
+  issue(gd_stage2, 2);
+  for (int s = 0; s < S; s += 4) {
+    sync();
+    issue(gd_stage3, s + 3);
+    compute(gd_stage0);
+    sync();
+    issue(gd_stage0, s + 4);
+    compute(gd_stage1);
+    sync();
+    issue(gd_stage1, s + 5);
+    compute(gd_stage2);
+    sync();
+    issue(gd_stage2, s + 6);
+    compute(gd_stage3);
+  }
+  // the three surplus loads land before the stages are reused below
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+
+  // ---- epilogue, one wave row (64 rows) at a time; tile row a in stage array a
+  float* sc[4] = {reinterpret_cast<float*>(gd_stage0), reinterpret_cast<float*>(gd_stage1),
+                  reinterpret_cast<float*>(gd_stage2), reinterpret_cast<float*>(gd_stage3)};
+  float bv[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) bv[b] = (float)bias[n0 + 64 * wn + 16 * b + l16];
+  constexpr int C4 = BN / 4;         // groups of 4 columns per row
+  constexpr int PER = 64 * C4 / 1024;  // groups per thread
+#pragma unroll 1
+  for (int part = 0; part < 4; ++part) {
+    if (wm == part) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            sc[a][(4 * gq + q) * LDC + 64 * wn + 16 * b + l16] = acc[a][b][q] + bv[b];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = tid + 1024 * j;
+      const int r = c / C4, c4 = 4 * (c - (c / C4) * C4);
+      const int row = m0 + 64 * part + r;
+      const float* src = r < 16 ? sc[0] : r < 32 ? sc[1] : r < 48 ? sc[2] : sc[3];
+      const float4 z = *reinterpret_cast<const float4*>(src + (r & 15) * LDC + c4);
+      if (row < M) {
+        float o0 = z.x, o1 = z.y, o2 = z.z, o3 = z.w;
+        if constexpr (EPI == kEpiGelu) {  // GELU(z) = z Phi(z) = 0.5 z (1 + erf(z / sqrt 2))
+          o0 = 0.5f * o0 * (1.f + erff(o0 * 0.70710678118654752f));
+          o1 = 0.5f * o1 * (1.f + erff(o1 * 0.70710678118654752f));
+          o2 = 0.5f * o2 * (1.f + erff(o2 * 0.70710678118654752f));
+          o3 = 0.5f * o3 * (1.f + erff(o3 * 0.70710678118654752f));
+        }
+        const int64_t off = (int64_t)row * N + n0 + c4;
+        if constexpr (EPI == kEpiResidual) {
+          const uint2 rw = *reinterpret_cast<const uint2*>(R + off);
+          o0 += __uint_as_float(rw.x << 16);
+          o1 += __uint_as_float(rw.x & 0xffff0000u);
+          o2 += __uint_as_float(rw.y << 16);
+          o3 += __uint_as_float(rw.y & 0xffff0000u);
+        }
+        *reinterpret_cast<uint2*>(D + off) = make_uint2(cvt_pk(o0, o1), cvt_pk(o2, o3));
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace afno
