@@ -440,13 +440,19 @@ __global__ void __launch_bounds__(1024) gemm_dma(const bf16* __restrict__ A,
         }
         const int64_t off = (int64_t)row * N + n0 + c4;
         if constexpr (EPI == kEpiResidual) {
-          const uint2 rw = *reinterpret_cast<const uint2*>(R + off);
+          // streamed once: non-temporal, so that the output and residual streams do not
+          // push the operands' k-slices out of the caches
+          const unsigned long long rq =
+              __builtin_nontemporal_load(reinterpret_cast<const unsigned long long*>(R + off));
+          const uint2 rw = make_uint2((uint32_t)rq, (uint32_t)(rq >> 32));
           o0 += __uint_as_float(rw.x << 16);
           o1 += __uint_as_float(rw.x & 0xffff0000u);
           o2 += __uint_as_float(rw.y << 16);
           o3 += __uint_as_float(rw.y & 0xffff0000u);
         }
-        *reinterpret_cast<uint2*>(D + off) = make_uint2(cvt_pk(o0, o1), cvt_pk(o2, o3));
+        __builtin_nontemporal_store(
+            (unsigned long long)cvt_pk(o0, o1) | ((unsigned long long)cvt_pk(o2, o3) << 32),
+            reinterpret_cast<unsigned long long*>(D + off));
       }
     }
     __syncthreads();
