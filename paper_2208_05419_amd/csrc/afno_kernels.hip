@@ -577,7 +577,8 @@ hipError_t launch_block(const Plan& pl, const BlockPtrs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(add_layer_norm_kernel, dim3(lng), dim3(256), 0, st, u, x,
                      static_cast<const bf16*>(a.ln2_g), static_cast<const bf16*>(a.ln2_b), v, w, M, C);
-  // row tiles of 256, padded to whole XCD rounds; column tiles of 256 where N allows
+  // row tiles of 256, padded to whole XCD rounds; column tiles of 256 (direct-to-LDS kernel)
+  // where N allows, else 128 (C a multiple of 128 makes K = C or 4 C a multiple of 128)
   const int64_t mbp = ((M + 255) / 256 + 7) / 8 * 8;
   auto gemm = [&](auto epi, const bf16* Am, const bf16* Bm, const bf16* bias, const bf16* Rm,
                   bf16* Dm, int N, int K) {
@@ -585,10 +586,6 @@ hipError_t launch_block(const Plan& pl, const BlockPtrs& a, hipStream_t st) {
     if (N % 256 == 0 && K % 128 == 0)
       hipLaunchKernelGGL((gemm_dma<E>), dim3((unsigned)(mbp * (N / 256))), dim3(1024), 0, st, Am,
                          Bm, bias, Rm, Dm, (int)M, N, K);
-    else if (N % 256 == 0)
-      hipLaunchKernelGGL((gemm_bf16<E, 256>), dim3((unsigned)(mbp * (N / 256))),
-                         dim3(GemmGeo<256>::NT), GemmGeo<256>::kBytes, st, Am, Bm, bias, Rm, Dm,
-                         (int)M, N, K);
     else
       hipLaunchKernelGGL((gemm_bf16<E, 128>), dim3((unsigned)(mbp * (N / 128))),
                          dim3(GemmGeo<128>::NT), GemmGeo<128>::kBytes, st, Am, Bm, bias, Rm, Dm,
@@ -617,9 +614,7 @@ hipError_t set_kernel_attributes() {
   AFNO_ATTR(column_bwd_kernel<float>)
   AFNO_ATTR(column_bwd_kernel<bf16>)
   AFNO_ATTR((gemm_bf16<kEpiGelu, 128>))
-  AFNO_ATTR((gemm_bf16<kEpiGelu, 256>))
   AFNO_ATTR((gemm_bf16<kEpiResidual, 128>))
-  AFNO_ATTR((gemm_bf16<kEpiResidual, 256>))
   AFNO_ATTR(wgrad_slab<64>)
   AFNO_ATTR(wgrad_slab<128>)
   AFNO_ATTR(wgrad_slab<192>)

@@ -151,13 +151,11 @@ __global__ void __launch_bounds__(256) transpose_bf16(const bf16* __restrict__ s
 
 enum { kEpiGelu = 0, kEpiResidual = 1 };
 
-// GEMM geometry: workgroup tile 256 x BN (rows x columns of D, BN = 128 or 256), k-stage 64
-// (two MFMA k-steps per barrier); 4 x (BN / 64) waves, each 64 x 64 (4 x 4 MFMA tiles of
-// 16 x 16).  LDS: two stages of the A (256 x 64) and B (BN x 64) slabs, rows padded to 72
-// elements (147 KB at BN = 256: one workgroup per CU); the epilogue reuses it for 64 rows of
-// fp32 at a time.  (Measured on the block's 64800 x 3072 x 768 and 64800 x 768 x 3072
-// products: 256 x 256 with 16 waves ahead of 256 x 128 with 8 and 128 x 128 with 4; 64-deep
-// stages 3-9 % ahead of 32-deep ones at this tile.)
+// GEMM geometry of the register-staged kernel (column counts N that are not a multiple of
+// 256): workgroup tile 256 x BN (rows x columns of D), k-stage 64 (two MFMA k-steps per
+// barrier); 4 x (BN / 64) waves, each 64 x 64 (4 x 4 MFMA tiles of 16 x 16).  LDS: two stages
+// of the A (256 x 64) and B (BN x 64) slabs, rows padded to 72 elements; the epilogue reuses
+// it for 64 rows of fp32 at a time.
 template <int BN>
 struct GemmGeo {
   static constexpr int BM = 256, BK = 64, LDK = BK + 8;
