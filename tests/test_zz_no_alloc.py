@@ -1,7 +1,9 @@
 """The allocation-free entry point (afno_filter_forward_noalloc) through the C ABI: on three
 calls in a row -- the 90 x 180 x 768 bf16 workload with B = 4 (about 102 MB of the library's
 128 MiB workspace), then smaller inputs that reuse the array the first call left behind -- its
-output equals afno_filter_forward's bit for bit (the same kernels on the same inputs)."""
+output equals afno_filter_forward's bit for bit (the same kernels on the same inputs).  It is
+for callers that cannot allocate, such as code under graph capture: recorded into a HIP graph
+and replayed, it gives the same bits again."""
 import numpy as np
 import pytest
 
@@ -63,3 +65,38 @@ def test_noalloc_torch_wrapper_writes_the_callers_out():
     ref = afno.filter_forward(x, w["w1"], w["b1"], w["w2"], w["b2"], wl.num_blocks, wl.lam, wl.keep)
     torch.cuda.synchronize()
     assert r is out and torch.equal(out, ref)
+
+
+def test_noalloc_replays_from_a_captured_graph():
+    """The allocation-free entry point recorded into a HIP graph (torch.cuda.graph) and replayed
+    three times, with eager work and synchronisations between the replays and new input values
+    before each: every replay's output equals an eager afno_filter_forward call on the same
+    input, bit for bit."""
+    wl = synth.Workload("noalloc_graph", 2, 30, 36, 192, 2, "bf16", 0.01, 1.0)
+    x = to_dev(synth.make_x(wl, seed=7), wl.dtype)
+    w = dev_weights(synth.make_weights(wl, seed=7), wl.dtype)
+    out = torch.empty_like(x)
+    s = torch.cuda.Stream()
+    # an eager call first: the library's one-time set-up (kernel attributes, the scratch
+    # array's address on this device) happens outside the capture
+    assert _raw(afno.afno_filter_forward_noalloc, x, w, out, wl, s.cuda_stream) == afno.AFNO_OK
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[noalloc graph] capture")
+    with torch.cuda.graph(g, stream=s):
+        rc = _raw(afno.afno_filter_forward_noalloc, x, w, out, wl, s.cuda_stream)
+    assert rc == afno.AFNO_OK, afno.afno_last_error()
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream().cuda_stream
+    for rep in range(3):
+        x.copy_(to_dev(synth.make_x(wl, seed=20 + rep), wl.dtype))  # eager work between replays
+        torch.cuda.synchronize()
+        say(f"[noalloc graph] replay {rep}")
+        g.replay()
+        torch.cuda.synchronize()
+        ref = torch.empty_like(x)
+        assert _raw(afno.afno_filter_forward, x, w, ref, wl, cur) == afno.AFNO_OK
+        torch.cuda.synchronize()
+        same = torch.equal(_bits(out), _bits(ref))
+        say(f"  replay {rep} bitwise equal to afno_filter_forward: {same}")
+        assert same
