@@ -67,7 +67,9 @@ enum {
  * Ownership: the caller owns every array; all are contiguous device memory on the
  * current device and must stay valid until the stream has finished the work.  The
  * library allocates a spectrum workspace of B*H*kept_w*C complex values (8 bytes each
- * for fp32, 4 for bf16) stream-ordered on `stream` and frees it stream-ordered.
+ * for fp32, 4 for bf16) stream-ordered on `stream` and frees it stream-ordered, from a
+ * memory pool of its own per device that keeps freed memory for later calls (so the
+ * largest workspaces in use at once stay allocated until the process ends).
  * The call is asynchronous: it enqueues on `stream` and returns.
  * B == 0 returns AFNO_OK without touching the GPU (x and out may then be NULL).
  * Errors: arguments are validated before any HIP call; on a non-OK return nothing

@@ -67,7 +67,8 @@ __global__ void __launch_bounds__(256) fill_zero_f32(float* __restrict__ p, int6
 // groups of eight, the group's 2 bs entries consecutive, eight modes per entry contiguous (one
 // 16-byte matrix-core operand for bf16).  The column (b, kw) holds modes (b KW + kw) HC ..
 // + HC - 1, HC = H16 rounded up to 32 (rows past H hold X = 0, do = dv = 0, so they add
-// nothing to the sums); mpad = B KW HC, a multiple of the bf16 product's 32-mode k-step.
+// nothing to the sums); mpad = B KW HC, a multiple of 32 (the slab product reads a chunk's
+// ragged last 64-mode step as zeros past its end).
 enum { kModeX = 0, kModeH = 1, kModeDo = 2, kModeDv = 3 };
 
 // tile rows 0 .. HC - 1 of the block's 2 bs entries -> dst groups m0 / 8 .., 8 rows per task
