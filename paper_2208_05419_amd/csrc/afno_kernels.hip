@@ -494,6 +494,18 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
                        dbias);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // dx = g + C2R(Sg): the W-axis inverse with g as the residual, first, while the gradient
+  // spectrum the column pass has just written may still sit in the last-level cache
+  T* dx = static_cast<T*>(a.dx);
+  if (pl.path != 1 && fast_row_available(pl.W, pl.C))
+    launch_row_inv_fast<T>(pl, Sg, g, dx, nullptr, 0, st);
+  else {
+    dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
+    hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, Sg, g, dx,
+                       nullptr, pl.row, 0);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   // weight gradients over all modes
   if (nslab > 0) {
     const dim3 sgrid((unsigned)(2 * nb * nslab));
@@ -517,17 +529,6 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
     hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kc, acc);
     hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
                        0, st, acc, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // dx = g + C2R(Sg): the W-axis inverse with g as the residual
-  T* dx = static_cast<T*>(a.dx);
-  if (pl.path != 1 && fast_row_available(pl.W, pl.C))
-    launch_row_inv_fast<T>(pl, Sg, g, dx, nullptr, 0, st);
-  else {
-    dim3 rgrid((unsigned)(pl.B * pl.H), (unsigned)(pl.C / pl.row.rc));
-    hipLaunchKernelGGL(row_c2r_kernel<T>, rgrid, dim3(kRowThreads), pl.row_lds, st, Sg, g, dx,
-                       nullptr, pl.row, 0);
   }
   return hipGetLastError();
 }

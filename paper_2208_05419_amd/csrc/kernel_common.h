@@ -165,6 +165,9 @@ __device__ __forceinline__ float softshrink(float v, float lam) {
   return v - __builtin_amdgcn_fmed3f(v, -lam, lam);
 }
 
+// cache-policy operand of the buffer intrinsics on gfx950: the non-temporal (streaming) hint
+constexpr int kNonTemporal = 2;
+
 // Raw buffer access: a per-workgroup base in a scalar resource descriptor, a 32-bit
 // per-lane byte offset and a wave-uniform byte offset, so addressing costs no 64-bit
 // vector arithmetic.  Accesses beyond `bytes` read 0 and do not write.
@@ -173,8 +176,9 @@ struct Buf {
   __device__ __forceinline__ Buf(const void* base, uint32_t bytes)
       : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                             0x00020000)) {}
+  template <int AUX = 0>
   __device__ __forceinline__ uint32_t ld32(uint32_t voff, uint32_t soff) const {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX);
   }
   __device__ __forceinline__ void st32(uint32_t v, uint32_t voff, uint32_t soff) const {
     __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
@@ -187,9 +191,10 @@ struct Buf {
     typedef uint32_t u2 __attribute__((ext_vector_type(2)));
     __builtin_amdgcn_raw_buffer_store_b64(u2{v.x, v.y}, r, voff, soff, 0);
   }
+  template <int AUX = 0>
   __device__ __forceinline__ void st128(uint4 v, uint32_t voff, uint32_t soff) const {
     typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-    __builtin_amdgcn_raw_buffer_store_b128(u4{v.x, v.y, v.z, v.w}, r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(u4{v.x, v.y, v.z, v.w}, r, voff, soff, AUX);
   }
 };
 __device__ __forceinline__ uint32_t buf_bytes(uint64_t n) {

@@ -479,11 +479,13 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
     voff[i] = (uint32_t)(w % SLAB) * 16u;
   }
   auto load = [&](uint4 (&r)[LW], int s) {
-    // the step's offset goes into the per-lane offset, which the range check covers
+    // the step's offset goes into the per-lane offset, which the range check covers; the factors
+  // are read once (non-temporal loads keep them from displacing other data in the caches)
     const uint32_t so = (uint32_t)s * (uint32_t)(SLAB * 16);
 #pragma unroll
     for (int i = 0; i < LW; ++i) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(opb[i] ? rb.r : ra.r, voff[i] + so, 0, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(opb[i] ? rb.r : ra.r, voff[i] + so, 0,
+                                                            kNonTemporal);
       r[i] = make_uint4(v[0], v[1], v[2], v[3]);
     }
   };

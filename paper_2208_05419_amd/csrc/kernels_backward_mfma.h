@@ -141,7 +141,8 @@ __device__ __forceinline__ void bwd_load_planes(bf16* P, const Buf& cb, int H, u
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const bool ok = task < XT && r0 + e < H;
-      const uint32_t wv = cb.ld32(ok ? c * 4u + (uint32_t)(r0 + e) * rsb : 0u, 0);
+      // non-temporal: each spectrum column is read once here (Sg is rewritten by P7 anyway)
+      const uint32_t wv = cb.ld32<kNonTemporal>(ok ? c * 4u + (uint32_t)(r0 + e) * rsb : 0u, 0);
       xv[u][e] = ok ? wv : 0u;
     }
   }
@@ -269,7 +270,11 @@ __device__ __forceinline__ void bwd_modes_out(const bf16* Rt, bf16* dst, int64_t
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       w[i] = (uint32_t)p[(2 * i) * G::kLdy] | ((uint32_t)p[(2 * i + 1) * G::kLdy] << 16);
-    *reinterpret_cast<uint4*>(dst + ((g0 + q) * NB2 + e) * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+    // non-temporal: 429 MB at the benchmark shape, read once, later, by the weight product;
+    // normal stores would push the spectra the next passes read out of the caches
+    typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u4v{w[0], w[1], w[2], w[3]},
+                                reinterpret_cast<u4v*>(dst + ((g0 + q) * NB2 + e) * 8));
   }
 }
 
