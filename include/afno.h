@@ -230,9 +230,9 @@ int afno_filter_backward(const void* x, const void* w1, const void* b1, const vo
  * records an event before its first kernel and after each of its four phases, on the
  * call's stream.  afno_profile_end waits for those events, writes the summed
  * milliseconds of each phase to kernel_ms[0..3] (0: operand preparation as a launch of its
- * own -- the block weights in MFMA fragment order and the H-axis DFT table; about 0 where
- * the column kernel takes none or where the preparation runs as extra workgroups of the
- * size-specialised W-axis forward launch; 1: W-axis forward transform; 2: column kernel,
+ * own -- the block weights in MFMA fragment order and the H-axis DFT table; exactly 0 where
+ * there is no such launch, the column kernel taking none or the preparation running as extra
+ * workgroups of the size-specialised W-axis forward launch; 1: W-axis forward transform; 2: column kernel,
  * H transforms + block MLP; 3: W-axis inverse transform + residual) and the number of timed calls to *calls, and
  * frees the events.  Calls beyond max_calls are not timed.
  * Returns AFNO_OK, AFNO_ERR_INVALID_ARG (max_calls <= 0, null output, or end without

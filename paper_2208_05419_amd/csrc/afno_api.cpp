@@ -580,6 +580,11 @@ int afno_profile_end(double* kernel_ms, int64_t* calls) {
     for (int k = 0; k < afno::kProfEvents - 1 && r == hipSuccess; ++k) {
       float ms = 0.f;
       r = hipEventElapsedTime(&ms, ev[k], ev[k + 1]);
+      if (k == 0 && r != hipSuccess) {  // no preparation launch of its own: ev[0] unrecorded
+        (void)hipGetLastError();
+        r = hipSuccess;
+        ms = 0.f;
+      }
       sum[k] += ms;
     }
     if (r != hipSuccess) rc = fail(AFNO_ERR_HIP, std::string("profile events: ") + hipGetErrorString(r));

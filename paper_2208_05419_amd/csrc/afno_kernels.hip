@@ -281,7 +281,10 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   if (col_mfma || col_fast)
     pj.wout = reinterpret_cast<typename FragWord<T>::type*>(static_cast<char*>(S) + pl.frag_offset);
   if (col_mfma) pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
-  if (ev) (void)hipEventRecord(ev[0], st);
+  // ev[0]: recorded only before a preparation launch of its own (a preparation inside the W-axis
+  // forward launch belongs to that phase; the profile counts an unrecorded ev[0] as zero)
+  const bool prep_launch = (pj.wout && !row_fast) || (sizeof(T) == 2 && col_hid);
+  if (ev && prep_launch) (void)hipEventRecord(ev[0], st);
   if (pj.wout && !row_fast) {
     const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp) + 255) / 256, 4096);
     hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
