@@ -392,7 +392,7 @@ size_t bwd_acc_floats(const Plan& pl) {
   int kc = 0;
   const int ns = wgrad_slab_chunks(pl, &kc);
   const size_t nb2 = 2 * (size_t)pl.bs;
-  return (size_t)(ns > 0 ? ns : 1) * 2 * pl.nb * nb2 * nb2 + 2 * (size_t)pl.nb * nb2;
+  return (size_t)(ns > 0 ? ns : 1) * 2 * pl.nb * nb2 * (nb2 + 1);
 }
 
 // The W-axis forward transform of x into S (no operand preparation).
@@ -441,24 +441,28 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   int kchunk = 0;
   const int nslab = wgrad_slab_chunks(pl, &kchunk);
   // the weight products' sums ([2][nb][2 bs][2 bs], or per chunk for the slab kernel), then
-  // the bias sums [2][nb][2 bs]
+  // the bias sums ([2][nb][2 bs], added by the column pass; per chunk [nslab][2][nb][2 bs] from
+  // the slab kernel, which takes them from the factors)
   const int64_t nprod = (int64_t)(nslab > 0 ? nslab : 1) * 2 * nb * nb2 * nb2;
-  float* dbias = acc + nprod;
+  float* bsums = acc + nprod;
+  float* dbias = nslab > 0 ? nullptr : bsums;
   const int64_t mpad = bwd_mpad(pl);
   const bool mfma = use_mfma_bwd(pl);
   hipError_t e = launch_row_forward<T>(pl, x, Sx, st);
   if (e == hipSuccess) e = launch_row_forward<T>(pl, g, Sg, st);
   if (e != hipSuccess) return e;
   const int64_t nw = (int64_t)2 * nb * bs * bs;
-  // cleared: the bias sums, and the products' sums where atomics accumulate them
-  float* zero_from = nslab > 0 ? dbias : acc;
-  const int64_t nzero = (int64_t)2 * nb * nb2 + (nslab > 0 ? 0 : nprod);
+  // cleared where atomics accumulate them: the products' and the bias sums (the slab kernel
+  // stores its sums, so nothing then)
+  float* zero_from = acc;
+  const int64_t nzero = nslab > 0 ? 0 : nprod + (int64_t)2 * nb * nb2;
   if (!mfma) {
     hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
                        dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
                        wt1, wt2, nb, bs);
-    hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
-                       dim3(256), 0, st, zero_from, nzero);
+    if (nzero > 0)
+      hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
+                         dim3(256), 0, st, zero_from, nzero);
   }
   if constexpr (sizeof(T) == 2) {
     if (mfma) {
@@ -514,15 +518,15 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
     const dim3 sgrid((unsigned)(2 * nb * nslab));
     if (nb2 == 64)
       hipLaunchKernelGGL(wgrad_slab<64>, sgrid, dim3(1024), 512 * 64, st,
-                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc, bsums);
     else if (nb2 == 128)
       hipLaunchKernelGGL(wgrad_slab<128>, sgrid, dim3(1024), 512 * 128, st,
-                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc, bsums);
     else
       hipLaunchKernelGGL(wgrad_slab<192>, sgrid, dim3(1024), 512 * 192, st,
-                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc);
+                         reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc, bsums);
     hipLaunchKernelGGL(wgrad_finalize_parts, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
-                       dim3(256), 0, st, acc, nslab, dbias, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
+                       dim3(256), 0, st, acc, nslab, bsums, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
   } else {
     // 64 x 64 output tiles, K split in chunks of whole 32-mode steps, fp32 atomics
     const int nt64 = (nb2 + 63) / 64;

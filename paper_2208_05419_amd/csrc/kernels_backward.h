@@ -109,12 +109,12 @@ __device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int
 }
 
 // column sums of the tile's first `rows` rows over its 2 bs entries, added to dst (fp32
-// atomics); the block has at least 2 bs threads
+// atomics; none where dst is null); the block has at least 2 bs threads
 template <typename T>
 __device__ __forceinline__ void tile_col_sums(const T* tile, int ldt, int rows, int nb2,
                                               float* dst) {
   const int e = threadIdx.x;
-  if (e < nb2) {
+  if (dst != nullptr && e < nb2) {
     float s = 0.f;
     for (int r = 0; r < rows; ++r) s += ld_f(tile + r * ldt + e);
     unsafeAtomicAdd(dst + e, s);  // device memory
@@ -183,7 +183,8 @@ __device__ __forceinline__ uint32_t mask_word(bool p0, bool p1, int lane) {
 // col_bwd_lds(p).  Sx: the forward spectrum of x; Sg: that of g, replaced by
 // G^-1-side gradient dX' = IDFT_H(dX) / c_kw (so that the forward C2R kernel's c_kw weights
 // give the unit-weight transpose); modes: the four per-mode factor tensors; dbias: [2][nb][2 bs]
-// fp32 sums (layer 0 db1, layer 1 db2).
+// fp32 sums (layer 0 db1, layer 1 db2), or null where the weight-product pass takes the bias
+// sums from the factors.
 template <typename T>
 __global__ void __launch_bounds__(kColMaxThreads)
 column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restrict__ w1,
@@ -287,7 +288,7 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
   }
   __syncthreads();
   write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDo), m0);
-  tile_col_sums<T>(tile, ldt, H16, nb2, dbias + ((int64_t)p.nb + blk) * nb2);
+  tile_col_sums<T>(tile, ldt, H16, nb2, dbias ? dbias + ((int64_t)p.nb + blk) * nb2 : nullptr);
 
   // ---- dv = (do W2^H) masked by v > 0; write dv
   if (active) block_gemm<T>(tile, ldt, wt2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -307,7 +308,7 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
   }
   __syncthreads();
   write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDv), m0);
-  tile_col_sums<T>(tile, ldt, H16, nb2, dbias + (int64_t)blk * nb2);
+  tile_col_sums<T>(tile, ldt, H16, nb2, dbias ? dbias + (int64_t)blk * nb2 : nullptr);
 
   // ---- dX = dv W1^H -> inverse H-DFT -> Sg column / c_kw
   if (active) block_gemm<T>(tile, ldt, wt1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -439,11 +440,16 @@ __global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ 
 // keeps two steps' bytes on the way from HBM.  16 waves as 4 x 4, each (NB2 / 64)^2 output
 // tiles of 16 x 16 (one workgroup per compute unit).  Words beyond the chunk's modes read 0
 // (buffer range check).  The chunk's sums go to part[chunk][layer][blk][r][s] (plain stores).
+// The same pass sums the second operand over the chunk's modes (do for dW2, dv for dW1: the
+// bias gradients db2, db1): each thread adds up the words it moves, in step order, and the
+// eight mode groups of an entry are added in a fixed order at the end, to
+// bpart[chunk][layer][blk][entry] -- so no atomics, and repeated calls give the same bits.
 // grid 2 nb nchunk (layer, block, chunk with block fastest), 1024 threads, dynamic LDS
 // 2 * 2 * 8 * NB2 * 16 bytes; kchunk a multiple of 64.
 template <int NB2>
 __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ modes, int64_t mpad,
-                                                   int nb, int kchunk, float* __restrict__ part) {
+                                                   int nb, int kchunk, float* __restrict__ part,
+                                                   float* __restrict__ bpart) {
   constexpr int T = NB2 / 64;       // output tiles per wave along each axis
   constexpr int SLAB = 8 * NB2;     // 16-byte words per operand and step
   constexpr int LW = 2 * SLAB / 1024;  // words each thread moves per step
@@ -489,9 +495,21 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
       r[i] = make_uint4(v[0], v[1], v[2], v[3]);
     }
   };
+  // per word moved: the sum of its eight modes, over all steps (used for the second operand)
+  float bsum[LW];
+#pragma unroll
+  for (int i = 0; i < LW; ++i) bsum[i] = 0.f;
   auto stash = [&](const uint4 (&r)[LW], int buf) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) slab_lds[buf * 2 * SLAB + tid + 1024 * i] = r[i];
+    for (int i = 0; i < LW; ++i) {
+      slab_lds[buf * 2 * SLAB + tid + 1024 * i] = r[i];
+      const uint32_t v[4] = {r[i].x, r[i].y, r[i].z, r[i].w};
+      float s8 = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        s8 += __uint_as_float(v[q] << 16) + __uint_as_float(v[q] & 0xffff0000u);
+      bsum[i] += s8;
+    }
   };
   f32x4 acc[T][T];
 #pragma unroll
@@ -536,6 +554,20 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
       __syncthreads();
     }
   }
+  // bias sums: word (group, entry) of the second operand's slab -> LDS, then per entry the
+  // eight groups in order (the slabs are no longer read: every product is behind a barrier)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(slab_lds);
+#pragma unroll
+  for (int i = 0; i < LW; ++i)
+    if (opb[i]) red[(tid + 1024 * i) % SLAB] = bsum[i];
+  __syncthreads();
+  if (tid < NB2) {
+    float sb = 0.f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) sb += red[q * NB2 + tid];
+    bpart[(((int64_t)chunk * 2 + layer) * nb + blk) * NB2 + tid] = sb;
+  }
   float* out = part + (((int64_t)chunk * 2 + layer) * nb + blk) * NB2 * NB2;
 #pragma unroll
   for (int i = 0; i < T; ++i)
@@ -547,10 +579,11 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
     }
 }
 
-// dW (re, im) from wgrad_slab's chunk sums (summed over the chunks here), and the bias sums
-// [2][nb][2 bs] copied to db1, db2.  Grid over 2 nb bs^2.
+// dW (re, im) from wgrad_slab's chunk sums, and db1, db2 from its chunk bias sums
+// bpart[chunk][2][nb][2 bs], each summed over the chunks here in chunk order.  Grid over
+// 2 nb bs^2.
 __global__ void __launch_bounds__(256) wgrad_finalize_parts(const float* __restrict__ part,
-                                                            int nchunk, const float* __restrict__ bias,
+                                                            int nchunk, const float* __restrict__ bpart,
                                                             int nb, int bs, float* __restrict__ dw1,
                                                             float* __restrict__ dw2,
                                                             float* __restrict__ db1,
@@ -576,7 +609,11 @@ __global__ void __launch_bounds__(256) wgrad_finalize_parts(const float* __restr
     float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
     d[0] = rr + ii;
     d[1] = ri - ir;
-    if (t < 2 * nbias) (t < nbias ? db1 : db2)[t < nbias ? t : t - nbias] = bias[t];
+    if (t < 2 * nbias) {
+      float sb = 0.f;
+      for (int c = 0; c < nchunk; ++c) sb += bpart[(int64_t)c * 2 * nbias + t];
+      (t < nbias ? db1 : db2)[t < nbias ? t : t - nbias] = sb;
+    }
   }
 }
 

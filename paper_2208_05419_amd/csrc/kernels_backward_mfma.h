@@ -278,12 +278,13 @@ __device__ __forceinline__ void bwd_modes_out(const bf16* Rt, bf16* dst, int64_t
   }
 }
 
-// column sums of a row-major tile over its HP rows, added to dst[entry] (fp32 atomics)
+// column sums of a row-major tile over its HP rows, added to dst[entry] (fp32 atomics; none
+// where dst is null)
 template <int HP, int BS>
 __device__ __forceinline__ void bwd_col_sums(const bf16* Rt, float* dst) {
   typedef MfmaCol<HP, BS> G;
   const int t = threadIdx.x;
-  if (t < 2 * BS) {
+  if (dst != nullptr && t < 2 * BS) {
     const uint16_t* p = reinterpret_cast<const uint16_t*>(Rt) + t;
     float s = 0.f;
 #pragma unroll 8
@@ -296,7 +297,8 @@ __device__ __forceinline__ void bwd_col_sums(const bf16* Rt, float* dst) {
 // Sx: spectrum of x; Sg: spectrum of g, replaced by IDFT_H(dX) / c_kw.  wfwd: fragments of
 // (w1, w2); wbwd: fragments of (conj(w2)^T, conj(w1)^T); dtab, dtab_lo: the DFT table and its
 // rounding remainders.  modes: the four
-// per-mode factor tensors; dbias: [2][nb][2 bs] fp32 sums (layer 0 db1, layer 1 db2).
+// per-mode factor tensors; dbias: [2][nb][2 bs] fp32 sums (layer 0 db1, layer 1 db2), or null
+// where the weight-product pass takes the bias sums from the factors.
 template <int HP, int BS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4* __restrict__ wfwd,
@@ -450,7 +452,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   }
   __syncthreads();
   bwd_modes_out<HP, BS>(R, tensor(2), g0);
-  bwd_col_sums<HP, BS>(R, dbias + ((int64_t)nb + blk) * NB2);
+  bwd_col_sums<HP, BS>(R, dbias ? dbias + ((int64_t)nb + blk) * NB2 : nullptr);
 
   // ---- P5: dh^T = W2x do^T, dv = dh where v > 0 -> DV[k][hidden]
   {
@@ -475,7 +477,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   }
   __syncthreads();
   bwd_modes_out<HP, BS>(R, tensor(3), g0);
-  bwd_col_sums<HP, BS>(R, dbias + (int64_t)blk * NB2);
+  bwd_col_sums<HP, BS>(R, dbias ? dbias + (int64_t)blk * NB2 : nullptr);
 
   // ---- P6: dX = DV W1x^T -> planes [rho][c][k]
   {

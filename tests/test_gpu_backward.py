@@ -212,3 +212,29 @@ def test_backward_at_the_benchmark_configuration():
     """The benchmark's backward: 90 x 180 x 768, 8 blocks of 96, bf16, B = 4, channel-scaled
     fields (the weight gradients sum over the batch, so all four samples are compared)."""
     _check_known(synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"])
+
+
+@pytest.mark.parametrize("path", ["auto", "generic"])
+def test_backward_repeats_bitwise_where_the_slab_product_runs(path):
+    """bf16 with 2 bs in {64, 128, 192}: the weight products and the bias sums are chunk sums
+    stored without atomics and added in a fixed order, so two calls give the same bits (on
+    the matrix-core and on the generic column kernel).  Random inputs: repeatability only."""
+    wl = synth.Workload("bwd_rep", 2, 90, 180, 768, 8, "bf16", 0.01, 1.0)
+    x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
+    g_st = synth.quantize(np.random.default_rng(77).standard_normal(x_st.shape), wl.dtype)
+    afno.set_kernel_path(afno.AFNO_PATH_AUTO if path == "auto" else afno.AFNO_PATH_GENERIC)
+    try:
+        w = dev_weights(w_st, wl.dtype)
+        x, g = _dev(x_st, wl.dtype), _dev(g_st, wl.dtype)
+        runs = []
+        for _ in range(2):
+            got = afno.filter_backward(x, w["w1"], w["b1"], w["w2"], w["b2"], g,
+                                       wl.num_blocks, wl.lam, wl.keep)
+            torch.cuda.synchronize()
+            runs.append({k: v.clone() for k, v in got.items()})
+    finally:
+        afno.set_kernel_path(afno.AFNO_PATH_AUTO)
+    for k in NAMES:
+        assert torch.equal(runs[0][k], runs[1][k]), k
+        assert bool(torch.isfinite(runs[0][k].float()).all()), k
+    say(f"backward {path}: two calls bitwise equal")
