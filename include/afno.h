@@ -212,14 +212,12 @@ int afno_filter_stage_hidden(const void* x, const void* w1, const void* b1, cons
  * No output may overlap an input or another output (AFNO_ERR_ALIAS).  The library
  * allocates stream-ordered workspace on `stream`: two spectra, the conjugate-transposed
  * weights, four per-mode factor tensors of nb * 2 bs * B * kept_w * ceil32(ceil16(H)) values
- * in dtype, and float32 sums (2 nb 2 bs (2 bs + 1) of them, once per mode chunk for bf16
- * with 2 bs in {64, 128, 192}).  B == 0 or nothing kept: dx = gout and zero weight and bias
- * gradients.  Errors as afno_filter_forward; AFNO_ERR_UNSUPPORTED also when a column of the
- * backward kernel (one tile of H x bs complex values plus two bit masks) does not fit the
- * LDS.  Reproducibility: for bf16 with 2 bs in {64, 128, 192} the weight and bias gradients
- * are chunk sums stored without atomics and added in a fixed order, so repeated calls give
- * the same bits; elsewhere they are sums of fp32 atomic additions, whose last bits may
- * differ between calls.
+ * in dtype, and float32 chunk sums (2 nb 2 bs (2 bs + 1) per chunk of modes, at most 64
+ * chunks).  B == 0 or nothing kept: dx = gout and zero weight and bias gradients.  Errors as
+ * afno_filter_forward; AFNO_ERR_UNSUPPORTED also when a column of the backward kernel (one
+ * tile of H x bs complex values plus two bit masks) does not fit the LDS.  Reproducibility:
+ * no atomics; the weight and bias gradients are chunk sums stored by the weight-product
+ * kernels and added in a fixed order, so repeated calls give the same bits.
  */
 int afno_filter_backward(const void* x, const void* w1, const void* b1, const void* w2,
                          const void* b2, const void* gout, int64_t B, int64_t H, int64_t W,

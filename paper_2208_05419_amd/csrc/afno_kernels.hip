@@ -386,13 +386,30 @@ int wgrad_slab_chunks(const Plan& pl, int* kchunk) {
   return (int)((mpad + kc - 1) / kc);
 }
 
-// floats of the backward's fp32 sums: the weight products' (per chunk for the slab kernel)
-// and the bias sums
+// mode chunks of the size-generic weight-product kernel: whole 32-mode steps, at most 32
+static int wgrad_generic_chunks(const Plan& pl, int* kchunk) {
+  const int64_t mpad = bwd_mpad(pl);
+  const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
+  const int64_t kc = ((mpad + nk - 1) / nk + 31) / 32 * 32;
+  *kchunk = (int)kc;
+  return (int)((mpad + kc - 1) / kc);
+}
+
+// the weight-product pass's mode chunks (and their length); *slab: the slab kernel runs
+static int wgrad_chunks(const Plan& pl, int* kchunk, bool* slab) {
+  const int ns = wgrad_slab_chunks(pl, kchunk);
+  *slab = ns > 0;
+  return ns > 0 ? ns : wgrad_generic_chunks(pl, kchunk);
+}
+
+// floats of the backward's fp32 chunk sums: per mode chunk, the weight products
+// [2][nb][2 bs][2 bs], then per chunk the bias sums [2][nb][2 bs]
 size_t bwd_acc_floats(const Plan& pl) {
   int kc = 0;
-  const int ns = wgrad_slab_chunks(pl, &kc);
+  bool slab = false;
+  const int nchunk = wgrad_chunks(pl, &kc, &slab);
   const size_t nb2 = 2 * (size_t)pl.bs;
-  return (size_t)(ns > 0 ? ns : 1) * 2 * pl.nb * nb2 * (nb2 + 1);
+  return (size_t)nchunk * 2 * pl.nb * nb2 * (nb2 + 1);
 }
 
 // The W-axis forward transform of x into S (no operand preparation).
@@ -411,15 +428,14 @@ static hipError_t launch_row_forward(const Plan& pl, const T* x, T* S, hipStream
 static void launch_col_bwd_mfma(const Plan& pl, const bf16* Sx, bf16* Sg, const uint4* wfwd,
                                 const uint4* wbwd, const uint4* tab, const uint4* tab_lo,
                                 const bf16* b1,
-                                const bf16* b2, bf16* modes, int64_t mpad, float* dbias,
-                                hipStream_t st) {
+                                const bf16* b2, bf16* modes, int64_t mpad, hipStream_t st) {
   const int hp = mfma_col_hp(pl.H);
   const dim3 grid((unsigned)(pl.B * pl.KW * pl.nb));
 #define AFNO_CASE(HP_, BS_)                                                                   \
   if (hp == HP_ && pl.bs == BS_) {                                                            \
     hipLaunchKernelGGL((column_bwd_mfma<HP_, BS_>), grid, dim3(512), (MfmaBwd<HP_, BS_>::kBytes), \
                        st, Sx, Sg, wfwd, wbwd, tab, tab_lo, b1, b2, (int)pl.H, (int)pl.C, (int)pl.KW,   \
-                       (int)pl.nb, (int)pl.kept_h, pl.col.lam, (int)pl.W, modes, mpad, dbias); \
+                       (int)pl.nb, (int)pl.kept_h, pl.col.lam, (int)pl.W, modes, mpad);      \
     return;                                                                                   \
   }
   AFNO_MFMA_COL_LIST(AFNO_CASE)
@@ -439,31 +455,21 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   float* acc = reinterpret_cast<float*>(ws + pl.bwd.acc_offset);
   const int nb = (int)pl.nb, bs = (int)pl.bs, nb2 = 2 * bs;
   int kchunk = 0;
-  const int nslab = wgrad_slab_chunks(pl, &kchunk);
-  // the weight products' sums ([2][nb][2 bs][2 bs], or per chunk for the slab kernel), then
-  // the bias sums ([2][nb][2 bs], added by the column pass; per chunk [nslab][2][nb][2 bs] from
-  // the slab kernel, which takes them from the factors)
-  const int64_t nprod = (int64_t)(nslab > 0 ? nslab : 1) * 2 * nb * nb2 * nb2;
-  float* bsums = acc + nprod;
-  float* dbias = nslab > 0 ? nullptr : bsums;
+  bool slab = false;
+  const int nchunk = wgrad_chunks(pl, &kchunk, &slab);
+  // the chunk sums of the weight products [nchunk][2][nb][2 bs][2 bs], then of the bias sums
+  // [nchunk][2][nb][2 bs]: stored, not accumulated, so nothing is cleared
+  float* bsums = acc + (int64_t)nchunk * 2 * nb * nb2 * nb2;
   const int64_t mpad = bwd_mpad(pl);
   const bool mfma = use_mfma_bwd(pl);
   hipError_t e = launch_row_forward<T>(pl, x, Sx, st);
   if (e == hipSuccess) e = launch_row_forward<T>(pl, g, Sg, st);
   if (e != hipSuccess) return e;
   const int64_t nw = (int64_t)2 * nb * bs * bs;
-  // cleared where atomics accumulate them: the products' and the bias sums (the slab kernel
-  // stores its sums, so nothing then)
-  float* zero_from = acc;
-  const int64_t nzero = nslab > 0 ? 0 : nprod + (int64_t)2 * nb * nb2;
-  if (!mfma) {
+  if (!mfma)
     hipLaunchKernelGGL(conj_transpose_weights<T>, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
                        dim3(256), 0, st, static_cast<const T*>(a.w1), static_cast<const T*>(a.w2),
                        wt1, wt2, nb, bs);
-    if (nzero > 0)
-      hipLaunchKernelGGL(fill_zero_f32<T>, dim3((unsigned)std::min<int64_t>((nzero + 255) / 256, 4096)),
-                         dim3(256), 0, st, zero_from, nzero);
-  }
   if constexpr (sizeof(T) == 2) {
     if (mfma) {
       typedef typename FragWord<T>::type Word;
@@ -480,9 +486,8 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
       PrepJob<T> pb{wt2, wt1, wbwd, nullptr, nb, bs, (int)pl.H, hp, 0, -1, 0};
       // everything that does not read wt1 / wt2 in one launch, then their fragments
       BwdPrep bp{pf, static_cast<const bf16*>(a.w1), static_cast<const bf16*>(a.w2), wt1, wt2,
-                 tab_lo, zero_from, nb, bs, (int)pl.H, hp, prep_words_host(pl, true, -1), ntab, nw,
-                 nzero};
-      const int64_t nall = bp.n_pf + bp.n_lo + bp.n_ct + bp.n_zero;
+                 tab_lo, nb, bs, (int)pl.H, hp, prep_words_host(pl, true, -1), ntab, nw};
+      const int64_t nall = bp.n_pf + bp.n_lo + bp.n_ct;
       hipLaunchKernelGGL(bwd_prep_kernel, dim3((unsigned)std::min<int64_t>((nall + 255) / 256, 4096)),
                          dim3(256), 0, st, bp);
       const unsigned gb = (unsigned)std::min<int64_t>((prep_words_host(pl, false, -1) + 255) / 256, 4096);
@@ -490,15 +495,14 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
       launch_col_bwd_mfma(pl, Sx, Sg, reinterpret_cast<const uint4*>(wfwd),
                           reinterpret_cast<const uint4*>(wbwd), tab, tab_lo,
                           static_cast<const T*>(a.b1),
-                          static_cast<const T*>(a.b2), modes, mpad, dbias, st);
+                          static_cast<const T*>(a.b2), modes, mpad, st);
     }
   }
   if (!mfma)
     hipLaunchKernelGGL(column_bwd_kernel<T>, dim3((unsigned)(pl.B * pl.KW * pl.nb)),
                        dim3(pl.col_threads), bwd_lds(pl), st, Sx, Sg, static_cast<const T*>(a.w1),
                        static_cast<const T*>(a.b1), static_cast<const T*>(a.w2),
-                       static_cast<const T*>(a.b2), wt1, wt2, pl.col, modes, mpad, (int)pl.W,
-                       dbias);
+                       static_cast<const T*>(a.b2), wt1, wt2, pl.col, modes, mpad, (int)pl.W);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // dx = g + C2R(Sg): the W-axis inverse with g as the residual, first, while the gradient
@@ -513,9 +517,9 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // weight gradients over all modes
-  if (nslab > 0) {
-    const dim3 sgrid((unsigned)(2 * nb * nslab));
+  // weight and bias gradients over all modes: chunk sums, then their sum in chunk order
+  if (slab) {
+    const dim3 sgrid((unsigned)(2 * nb * nchunk));
     if (nb2 == 64)
       hipLaunchKernelGGL(wgrad_slab<64>, sgrid, dim3(1024), 512 * 64, st,
                          reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc, bsums);
@@ -525,18 +529,15 @@ static hipError_t launch_bwd(const Plan& pl, const BwdPtrs& a, hipStream_t st) {
     else
       hipLaunchKernelGGL(wgrad_slab<192>, sgrid, dim3(1024), 512 * 192, st,
                          reinterpret_cast<const bf16*>(modes), mpad, nb, kchunk, acc, bsums);
-    hipLaunchKernelGGL(wgrad_finalize_parts, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
-                       dim3(256), 0, st, acc, nslab, bsums, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
   } else {
-    // 64 x 64 output tiles, K split in chunks of whole 32-mode steps, fp32 atomics
+    // 64 x 64 output tiles, chunks of whole 32-mode steps
     const int nt64 = (nb2 + 63) / 64;
-    const int64_t nk = std::max<int64_t>(1, std::min<int64_t>(32, (mpad + 4095) / 4096));
-    const int kc = (int)(((mpad + nk - 1) / nk + 31) / 32 * 32);
-    const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)((mpad + kc - 1) / kc));
-    hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kc, acc);
-    hipLaunchKernelGGL(wgrad_finalize, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)), dim3(256),
-                       0, st, acc, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
+    const dim3 wgrid((unsigned)(2 * nb * nt64 * nt64), (unsigned)nchunk);
+    hipLaunchKernelGGL(wgrad_kernel<T>, wgrid, dim3(256), 0, st, modes, mpad, nb, bs, kchunk, acc,
+                       bsums);
   }
+  hipLaunchKernelGGL(wgrad_finalize_parts, dim3((unsigned)std::min<int64_t>((nw + 255) / 256, 4096)),
+                     dim3(256), 0, st, acc, nchunk, bsums, nb, bs, a.dw1, a.dw2, a.db1, a.db2);
   return hipGetLastError();
 }
 

@@ -17,10 +17,12 @@
 //
 // Passes: the forward W-axis kernel on x and on g (spectra Sx, Sg); a backward column kernel
 // per (b, kw, block) recomputes X, h and both masks, transforms the gradient column and runs
-// the two conjugate-transposed products, writing dX's inverse back into Sg, the per-mode
-// factors X, h, do, dv to HBM in 8-mode groups and the bias sums (db2 = sum do, db1 = sum dv)
-// by fp32 atomics; wgrad_kernel reduces the weight gradients over all modes on the matrix
-// cores; the forward W-axis inverse kernel with g as its residual gives dx.  This header
+// the two conjugate-transposed products, writing dX's inverse back into Sg and the per-mode
+// factors X, h, do, dv to HBM in 8-mode groups; a weight-product kernel (wgrad_slab for bf16
+// with 2 bs in {64, 128, 192}, else wgrad_kernel) forms the weight and bias gradients from the
+// factors on the matrix cores as chunk sums, which wgrad_finalize_parts adds in a fixed order
+// (no floating-point atomics: repeated calls give the same bits); the forward W-axis inverse kernel
+// with g as its residual gives dx.  This header
 // holds the size-generic column kernel (any dtype, H <= 192); kernels_backward_mfma.h the bf16
 // one for H <= 96 with the H transforms on the matrix cores.
 #pragma once
@@ -108,19 +110,6 @@ __device__ __forceinline__ void write_modes(const T* tile, int ldt, int H16, int
   }
 }
 
-// column sums of the tile's first `rows` rows over its 2 bs entries, added to dst (fp32
-// atomics; none where dst is null); the block has at least 2 bs threads
-template <typename T>
-__device__ __forceinline__ void tile_col_sums(const T* tile, int ldt, int rows, int nb2,
-                                              float* dst) {
-  const int e = threadIdx.x;
-  if (dst != nullptr && e < nb2) {
-    float s = 0.f;
-    for (int r = 0; r < rows; ++r) s += ld_f(tile + r * ldt + e);
-    unsafeAtomicAdd(dst + e, s);  // device memory
-  }
-}
-
 // one column's rows h < H from S into the tile (times scale), padding rows zero
 template <typename T>
 __device__ __forceinline__ void load_column(T* tile, const T* col, int64_t row_stride, int ldt,
@@ -182,15 +171,14 @@ __device__ __forceinline__ uint32_t mask_word(bool p0, bool p1, int lane) {
 // grid B * KW * nb (block index fastest), block 64 * max(bs / 16, 4), dynamic LDS
 // col_bwd_lds(p).  Sx: the forward spectrum of x; Sg: that of g, replaced by
 // G^-1-side gradient dX' = IDFT_H(dX) / c_kw (so that the forward C2R kernel's c_kw weights
-// give the unit-weight transpose); modes: the four per-mode factor tensors; dbias: [2][nb][2 bs]
-// fp32 sums (layer 0 db1, layer 1 db2), or null where the weight-product pass takes the bias
-// sums from the factors.
+// give the unit-weight transpose); modes: the four per-mode factor tensors (the weight-product
+// pass takes the weight and bias gradients from them).
 template <typename T>
 __global__ void __launch_bounds__(kColMaxThreads)
 column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restrict__ w1,
                   const T* __restrict__ b1, const T* __restrict__ w2, const T* __restrict__ b2,
                   const T* __restrict__ wt1, const T* __restrict__ wt2, ColParams p,
-                  T* __restrict__ modes, int64_t mpad, int W, float* __restrict__ dbias) {
+                  T* __restrict__ modes, int64_t mpad, int W) {
   extern __shared__ float4 smem_raw[];
   T* tile = reinterpret_cast<T*>(smem_raw);
   const size_t mk_bytes = col_bwd_mask_bytes(p);
@@ -288,7 +276,6 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
   }
   __syncthreads();
   write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDo), m0);
-  tile_col_sums<T>(tile, ldt, H16, nb2, dbias ? dbias + ((int64_t)p.nb + blk) * nb2 : nullptr);
 
   // ---- dv = (do W2^H) masked by v > 0; write dv
   if (active) block_gemm<T>(tile, ldt, wt2 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -308,7 +295,6 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
   }
   __syncthreads();
   write_modes<T>(tile, ldt, H16, HC, bs, mode_tensor(kModeDv), m0);
-  tile_col_sums<T>(tile, ldt, H16, nb2, dbias ? dbias + (int64_t)blk * nb2 : nullptr);
 
   // ---- dX = dv W1^H -> inverse H-DFT -> Sg column / c_kw
   if (active) block_gemm<T>(tile, ldt, wt1 + (int64_t)blk * bs * bs * 2, bs, bs, mt, live, wave, lane, acc);
@@ -338,14 +324,18 @@ column_bwd_kernel(const T* __restrict__ Sx, T* __restrict__ Sg, const T* __restr
 }
 
 // Weight-gradient products over all modes: for layer 0 (dW1) A = X, B = dv; for layer 1
-// (dW2) A = h, B = do; acc[layer][blk][r][s] += sum over the workgroup's mode range of
-// A[r][m] B[s][m] (r, s the 2 bs real entries, (c, rho) interleaved), fp32 atomics.
-// grid (2 nb tiles64^2, ceil(mpad / kchunk)), 256 threads: four waves with 32 x 32 each of
-// a 64 x 64 output tile; kchunk a multiple of 32.
+// (dW2) A = h, B = do; part[chunk][layer][blk][r][s] = sum over the chunk's modes of
+// A[r][m] B[s][m] (r, s the 2 bs real entries, (c, rho) interleaved), and
+// bpart[chunk][layer][blk][s] = sum of B[s][m] (the bias gradients db1, db2): plain stores,
+// one workgroup per output value and chunk, summed over the chunks by wgrad_finalize_parts in
+// chunk order, so repeated calls give the same bits.
+// grid (2 nb tiles64^2, nchunk = ceil(mpad / kchunk)), 256 threads: four waves with 32 x 32
+// each of a 64 x 64 output tile; kchunk a multiple of 32.
 template <typename T>
 __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes, int64_t mpad,
                                                     int nb, int bs, int kchunk,
-                                                    float* __restrict__ acc_out) {
+                                                    float* __restrict__ part,
+                                                    float* __restrict__ bpart) {
   typedef Mma<T> M;
   const int nb2 = 2 * bs;
   const int nt64 = (nb2 + 63) / 64;
@@ -367,6 +357,10 @@ __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes,
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bool rv[2] = {r0 < nb2, r0 + 16 < nb2}, sv[2] = {s0 < nb2, s0 + 16 < nb2};
   const int l16 = lane & 15, gq = lane >> 4;
+  // the two waves of the first row tile also sum their B fragments: entries s0 + 16 j + l16,
+  // this lane's modes of each k-step
+  const bool bias_wave = tr == 0 && (wave >> 1) == 0;
+  float bsum[2] = {0.f, 0.f};
   for (int64_t k = k0; k < k1; k += M::kK) {
     typename M::Frag a[2], bfr[2];
 #pragma unroll
@@ -387,8 +381,32 @@ __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes,
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = M::mma(a[i], bfr[j], acc[i][j]);
+    if (bias_wave) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        if constexpr (sizeof(T) == 2) {
+          float s8 = 0.f;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) s8 += (float)bfr[j][q];
+          bsum[j] += s8;
+        } else {
+          bsum[j] += bfr[j];
+        }
+      }
+    }
   }
-  float* out = acc_out + ((int64_t)layer * nb + blk) * nb2 * nb2;
+  const int64_t slot = ((int64_t)blockIdx.y * 2 + layer) * nb + blk;
+  if (bias_wave) {
+    // the four lane groups hold different modes of the same entry: a fixed butterfly
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float v = bsum[j];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (gq == 0 && sv[j]) bpart[slot * nb2 + s0 + 16 * j + l16] = v;
+    }
+  }
+  float* out = part + slot * nb2 * nb2;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -398,38 +416,9 @@ __global__ void __launch_bounds__(256) wgrad_kernel(const T* __restrict__ modes,
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r = r0 + 16 * i + 4 * gq + q;
-        unsafeAtomicAdd(out + (int64_t)r * nb2 + s, acc[i][j][q]);  // device memory
+        out[(int64_t)r * nb2 + s] = acc[i][j][q];
       }
     }
-}
-
-// dW (re, im) from the real-entry products: for entries r = (i, rho), s = (j, sigma),
-// dW[i][j] = (P[(i,0)][(j,0)] + P[(i,1)][(j,1)], P[(i,0)][(j,1)] - P[(i,1)][(j,0)])
-// (conj(a) b summed); the bias sums [2][nb][2 bs] after the products copy to db1, db2.
-// Grid over 2 nb bs^2.
-__global__ void __launch_bounds__(256) wgrad_finalize(const float* __restrict__ acc_in, int nb,
-                                                      int bs, float* __restrict__ dw1,
-                                                      float* __restrict__ dw2,
-                                                      float* __restrict__ db1,
-                                                      float* __restrict__ db2) {
-  const int nb2 = 2 * bs;
-  const int64_t n = (int64_t)nb * bs * bs;
-  const int64_t nbias = (int64_t)nb * nb2;
-  const float* bias = acc_in + (int64_t)2 * nb * nb2 * nb2;
-  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < 2 * n;
-       t += (int64_t)gridDim.x * blockDim.x) {
-    const int layer = t >= n ? 1 : 0;
-    const int64_t u = t - layer * n;
-    const int64_t k = u / ((int64_t)bs * bs);
-    const int r = (int)(u - k * bs * bs), i = r / bs, j = r % bs;
-    const float* P = acc_in + ((int64_t)layer * nb + k) * nb2 * nb2;
-    const float rr = P[(2 * i) * nb2 + 2 * j], ii = P[(2 * i + 1) * nb2 + 2 * j + 1];
-    const float ri = P[(2 * i) * nb2 + 2 * j + 1], ir = P[(2 * i + 1) * nb2 + 2 * j];
-    float* d = (layer ? dw2 : dw1) + ((k * bs + i) * bs + j) * 2;
-    d[0] = rr + ii;
-    d[1] = ri - ir;
-    if (t < 2 * nbias) (t < nbias ? db1 : db2)[t < nbias ? t : t - nbias] = bias[t];
-  }
 }
 
 // bf16 weight-gradient products for 2 bs = NB2 a multiple of 64: one workgroup per (layer,
@@ -503,12 +492,14 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
 #pragma unroll
     for (int i = 0; i < LW; ++i) {
       slab_lds[buf * 2 * SLAB + tid + 1024 * i] = r[i];
-      const uint32_t v[4] = {r[i].x, r[i].y, r[i].z, r[i].w};
-      float s8 = 0.f;
+      if (opb[i]) {  // wave-uniform
+        const uint32_t v[4] = {r[i].x, r[i].y, r[i].z, r[i].w};
+        float s8 = 0.f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        s8 += __uint_as_float(v[q] << 16) + __uint_as_float(v[q] & 0xffff0000u);
-      bsum[i] += s8;
+        for (int q = 0; q < 4; ++q)
+          s8 += __uint_as_float(v[q] << 16) + __uint_as_float(v[q] & 0xffff0000u);
+        bsum[i] += s8;
+      }
     }
   };
   f32x4 acc[T][T];
@@ -579,8 +570,10 @@ __global__ void __launch_bounds__(1024) wgrad_slab(const bf16* __restrict__ mode
     }
 }
 
-// dW (re, im) from wgrad_slab's chunk sums, and db1, db2 from its chunk bias sums
-// bpart[chunk][2][nb][2 bs], each summed over the chunks here in chunk order.  Grid over
+// dW (re, im) from the weight-product kernels' chunk sums part[chunk][2][nb][2 bs][2 bs]: for
+// entries r = (i, rho), s = (j, sigma), dW[i][j] = (P[(i,0)][(j,0)] + P[(i,1)][(j,1)],
+// P[(i,0)][(j,1)] - P[(i,1)][(j,0)]) (conj(a) b summed); db1, db2 from the chunk bias sums
+// bpart[chunk][2][nb][2 bs]; each summed over the chunks here in chunk order.  Grid over
 // 2 nb bs^2.
 __global__ void __launch_bounds__(256) wgrad_finalize_parts(const float* __restrict__ part,
                                                             int nchunk, const float* __restrict__ bpart,

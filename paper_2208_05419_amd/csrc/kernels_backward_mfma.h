@@ -65,31 +65,27 @@ __device__ __forceinline__ uint4 dft_table_word_lo(int64_t i, int H, int HP) {
 
 // The backward's independent preparations in one launch, index ranges in turn: the forward
 // operands (block weights in fragment order and the DFT table, PrepJob pf), the table's
-// rounding remainders, the conjugate-transposed weights, and the cleared sums.  The
-// fragments of the conjugate-transposed weights read wt1 / wt2 and follow in a launch of
-// their own.
+// rounding remainders, and the conjugate-transposed weights.  The fragments of the
+// conjugate-transposed weights read wt1 / wt2 and follow in a launch of their own.
 struct BwdPrep {
   PrepJob<bf16> pf;
   const bf16 *w1, *w2;
   bf16 *wt1, *wt2;
   uint4* tab_lo;
-  float* zero;
   int nb, bs, H, HP;
-  int64_t n_pf, n_lo, n_ct, n_zero;
+  int64_t n_pf, n_lo, n_ct;
 };
 
 __global__ void __launch_bounds__(256) bwd_prep_kernel(BwdPrep p) {
-  const int64_t e1 = p.n_pf, e2 = e1 + p.n_lo, e3 = e2 + p.n_ct, e4 = e3 + p.n_zero;
-  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < e4;
+  const int64_t e1 = p.n_pf, e2 = e1 + p.n_lo, e3 = e2 + p.n_ct;
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < e3;
        t += (int64_t)gridDim.x * blockDim.x) {
     if (t < e1)
-      prep_operands<bf16>(t, e4, p.pf, nullptr);  // this word only (the next: t + e4 >= e1)
+      prep_operands<bf16>(t, e3, p.pf, nullptr);  // this word only (the next: t + e3 >= e1)
     else if (t < e2)
       p.tab_lo[t - e1] = dft_table_word_lo(t - e1, p.H, p.HP);
-    else if (t < e3)
-      conj_transpose_one<bf16>(t - e2, p.w1, p.w2, p.wt1, p.wt2, p.nb, p.bs);
     else
-      p.zero[t - e3] = 0.f;
+      conj_transpose_one<bf16>(t - e2, p.w1, p.w2, p.wt1, p.wt2, p.nb, p.bs);
   }
 }
 
@@ -278,34 +274,18 @@ __device__ __forceinline__ void bwd_modes_out(const bf16* Rt, bf16* dst, int64_t
   }
 }
 
-// column sums of a row-major tile over its HP rows, added to dst[entry] (fp32 atomics; none
-// where dst is null)
-template <int HP, int BS>
-__device__ __forceinline__ void bwd_col_sums(const bf16* Rt, float* dst) {
-  typedef MfmaCol<HP, BS> G;
-  const int t = threadIdx.x;
-  if (dst != nullptr && t < 2 * BS) {
-    const uint16_t* p = reinterpret_cast<const uint16_t*>(Rt) + t;
-    float s = 0.f;
-#pragma unroll 8
-    for (int k = 0; k < HP; ++k) s += __uint_as_float((uint32_t)p[k * G::kLdy] << 16);
-    unsafeAtomicAdd(dst + t, s);  // device memory
-  }
-}
-
 // grid B * KW * nb (block index fastest), 512 threads, dynamic LDS MfmaBwd<HP, BS>::kBytes.
 // Sx: spectrum of x; Sg: spectrum of g, replaced by IDFT_H(dX) / c_kw.  wfwd: fragments of
 // (w1, w2); wbwd: fragments of (conj(w2)^T, conj(w1)^T); dtab, dtab_lo: the DFT table and its
 // rounding remainders.  modes: the four
-// per-mode factor tensors; dbias: [2][nb][2 bs] fp32 sums (layer 0 db1, layer 1 db2), or null
-// where the weight-product pass takes the bias sums from the factors.
+// per-mode factor tensors (the weight-product pass takes the weight and bias gradients from
+// them).
 template <int HP, int BS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4* __restrict__ wfwd,
                 const uint4* __restrict__ wbwd, const uint4* __restrict__ dtab,
                 const uint4* __restrict__ dtab_lo, const bf16* __restrict__ b1, const bf16* __restrict__ b2, int H, int C, int KW,
-                int nb, int kept_h, float lam, int W, bf16* __restrict__ modes, int64_t mpad,
-                float* __restrict__ dbias) {
+                int nb, int kept_h, float lam, int W, bf16* __restrict__ modes, int64_t mpad) {
   typedef MfmaCol<HP, BS> G;
   typedef MfmaBwd<HP, BS> Q;
   constexpr int NB2 = Q::NB2, NW1 = Q::NW1, NW2 = Q::NW2;
@@ -452,7 +432,6 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   }
   __syncthreads();
   bwd_modes_out<HP, BS>(R, tensor(2), g0);
-  bwd_col_sums<HP, BS>(R, dbias ? dbias + ((int64_t)nb + blk) * NB2 : nullptr);
 
   // ---- P5: dh^T = W2x do^T, dv = dh where v > 0 -> DV[k][hidden]
   {
@@ -460,7 +439,7 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
     f32x4 acc[G::TMW][G::TNW];
     bwd_prod_wt<HP, BS>(Buf(wbwd + blk * kBlockWords, (uint32_t)(kBlockWords * 16)), 0, R, lane,
                         twm, twn, acc);
-    __syncthreads();  // DO read by every wave (products, modes, sums)
+    __syncthreads();  // DO read by every wave (products, modes)
 #pragma unroll
     for (int m = 0; m < G::TMW; ++m)
 #pragma unroll
@@ -477,7 +456,6 @@ column_bwd_mfma(const bf16* __restrict__ Sx, bf16* __restrict__ Sg, const uint4*
   }
   __syncthreads();
   bwd_modes_out<HP, BS>(R, tensor(3), g0);
-  bwd_col_sums<HP, BS>(R, dbias ? dbias + (int64_t)blk * NB2 : nullptr);
 
   // ---- P6: dX = DV W1x^T -> planes [rho][c][k]
   {

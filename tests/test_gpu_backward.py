@@ -214,12 +214,14 @@ def test_backward_at_the_benchmark_configuration():
     _check_known(synth.WORKLOADS["afno90x180_c768_nb8_bf16_b4"])
 
 
-@pytest.mark.parametrize("path", ["auto", "generic"])
-def test_backward_repeats_bitwise_where_the_slab_product_runs(path):
-    """bf16 with 2 bs in {64, 128, 192}: the weight products and the bias sums are chunk sums
-    stored without atomics and added in a fixed order, so two calls give the same bits (on
-    the matrix-core and on the generic column kernel).  Random inputs: repeatability only."""
-    wl = synth.Workload("bwd_rep", 2, 90, 180, 768, 8, "bf16", 0.01, 1.0)
+@pytest.mark.parametrize("path,dtype,nb", [("auto", "bf16", 8), ("generic", "bf16", 8),
+                                           ("auto", "fp32", 8), ("auto", "bf16", 6)])
+def test_backward_repeats_bitwise(path, dtype, nb):
+    """The weight and bias gradients are chunk sums stored without atomics and added in a fixed
+    order, so two calls give the same bits: the slab weight product after the matrix-core and
+    after the generic column kernel (bf16, 96-channel blocks), the size-generic weight product
+    (fp32; bf16 with 128-channel blocks).  Random inputs: repeatability only."""
+    wl = synth.Workload("bwd_rep", 2, 90, 180, 768, nb, dtype, 0.01, 1.0)
     x_st, w_st = synth.make_x(wl), synth.make_weights(wl)
     g_st = synth.quantize(np.random.default_rng(77).standard_normal(x_st.shape), wl.dtype)
     afno.set_kernel_path(afno.AFNO_PATH_AUTO if path == "auto" else afno.AFNO_PATH_GENERIC)
@@ -237,4 +239,4 @@ def test_backward_repeats_bitwise_where_the_slab_product_runs(path):
     for k in NAMES:
         assert torch.equal(runs[0][k], runs[1][k]), k
         assert bool(torch.isfinite(runs[0][k].float()).all()), k
-    say(f"backward {path}: two calls bitwise equal")
+    say(f"backward {path} {dtype} nb={nb}: two calls bitwise equal")
