@@ -56,7 +56,12 @@ static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h, int kp
          (with_tab ? (kp > 0 ? kept_table_tasks(hp, kp) : dft_table_tasks(hp, kept_h)) : 0);
 }
 
-#define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 24, 15, 16)
+// Size-specialised W-axis kernels: (W, N1, N2, NP), W = N1 N2 split into an N2-point register
+// stage and an N1-point stage after the LDS exchange, NP complex signals per workgroup.  The
+// splits are the measured fastest per direction (W = 180: forward 12 x 15, inverse 15 x 12;
+// W = 360: 15 x 24 both ways); the slice width NP is the same in both lists.
+#define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 15, 24, 16)
+#define AFNO_ROW_INV_LIST(X) X(32, 8, 4, 32) X(180, 15, 12, 32) X(360, 15, 24, 16)
 bool fast_row_available(int64_t W, int64_t C) {
 #define AFNO_CASE(w, n1, n2, np) if (W == w) return C % (2 * np) == 0;
   AFNO_ROW_FAST_LIST(AFNO_CASE)
@@ -101,7 +106,7 @@ static void launch_row_inv_fast(const Plan& pl, const T* S, const T* x, T* out, 
                        S, x, out, dst, (int)pl.C, (int)pl.KW, sc, mode, (int64_t)gx);     \
     return;                                                                               \
   }
-  AFNO_ROW_FAST_LIST(AFNO_CASE)
+  AFNO_ROW_INV_LIST(AFNO_CASE)
 #undef AFNO_CASE
 }
 

@@ -195,56 +195,31 @@ row_r2c_fast(const T* __restrict__ x, T* __restrict__ S, int C, int KW, float sc
       F[(k2 * N1 + j) * NP + p] = k2 == 0 ? v[0] : twiddle<false>(v[k2], tw, j * k2);
   }
   __syncthreads();
-  if constexpr (N1 >= 24) {
-    // Long second-stage transforms: one task per (signal, residue class q), its N1-point
-    // DFT written back in place (slot (q, k1) of signal p then holds Z[q + N2 k1]), then the
-    // two real spectra separate from Z[k] and Z[W - k] with one task per (bin, signal), so
-    // every thread takes part in both steps.
-    for (int task = tid; task < NP * N2; task += NT) {
-      const int p = task % NP, q = task / NP;
-      float2 a[N1];
+  // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
+  // for every k of both residue classes, so the two real spectra separate in registers.
+  constexpr int NPT = N2 / 2 + 1;
+  for (int task = tid; task < NP * NPT; task += NT) {
+    const int p = task % NP, q = task / NP;
+    const int qa = q, qb = (N2 - q) % N2;
+    float2 a[N1], b[N1];
 #pragma unroll
-      for (int j = 0; j < N1; ++j) a[j] = F[(q * N1 + j) * NP + p];
-      DftReg<N1, false>::run(a);
-#pragma unroll
-      for (int k1 = 0; k1 < N1; ++k1) F[(q * N1 + k1) * NP + p] = a[k1];
+    for (int j = 0; j < N1; ++j) {
+      a[j] = F[(qa * N1 + j) * NP + p];
+      b[j] = F[(qb * N1 + j) * NP + p];
     }
-    __syncthreads();
-    const int nk = KW < W / 2 + 1 ? KW : W / 2 + 1;
-    for (int i = tid; i < nk * NP; i += NT) {
-      const int p = i % NP, k = i / NP;
-      const int km = k == 0 ? 0 : W - k;
-      const float2 z = F[((k % N2) * N1 + k / N2) * NP + p];
-      const float2 zm = F[((km % N2) * N1 + km / N2) * NP + p];
-      st_cpair(sb, (const T*)nullptr, 4 * p * es + k * srow, 0, split_pair(z, zm, scale));
-    }
-  } else {
-    // One task per pair of residues {q, N2 - q}: it holds Z[k] and its partner Z[W - k]
-    // for every k of both residue classes, so the two real spectra separate in registers.
-    constexpr int NPT = N2 / 2 + 1;
-    for (int task = tid; task < NP * NPT; task += NT) {
-      const int p = task % NP, q = task / NP;
-      const int qa = q, qb = (N2 - q) % N2;
-      float2 a[N1], b[N1];
+    DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
+    DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
+    const uint32_t va = 4 * p * es + qa * srow, vb = 4 * p * es + qb * srow;
 #pragma unroll
-      for (int j = 0; j < N1; ++j) {
-        a[j] = F[(qa * N1 + j) * NP + p];
-        b[j] = F[(qb * N1 + j) * NP + p];
-      }
-      DftReg<N1, false>::run(a);  // a[k1] = Z[qa + N2 k1]
-      DftReg<N1, false>::run(b);  // b[k1] = Z[qb + N2 k1]
-      const uint32_t va = 4 * p * es + qa * srow, vb = 4 * p * es + qb * srow;
-#pragma unroll
-      for (int k1 = 0; k1 < N1; ++k1) {
-        // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
-        const int ka = qa + N2 * k1;
-        const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
-        if (ka <= W / 2 && ka < KW)
-          st_cpair(sb, (const T*)nullptr, va, N2 * k1 * srow, split_pair(a[k1], zam, scale));
-        const int kb = qb + N2 * k1;
-        if (qb != qa && kb <= W / 2 && kb < KW)
-          st_cpair(sb, (const T*)nullptr, vb, N2 * k1 * srow, split_pair(b[k1], a[N1 - 1 - k1], scale));
-      }
+    for (int k1 = 0; k1 < N1; ++k1) {
+      // partner of qa + N2 k1: N2 (N1 - k1) for q = 0, else qb + N2 (N1 - 1 - k1)
+      const int ka = qa + N2 * k1;
+      const float2 zam = (q == 0) ? a[(N1 - k1) % N1] : b[N1 - 1 - k1];
+      if (ka <= W / 2 && ka < KW)
+        st_cpair(sb, (const T*)nullptr, va, N2 * k1 * srow, split_pair(a[k1], zam, scale));
+      const int kb = qb + N2 * k1;
+      if (qb != qa && kb <= W / 2 && kb < KW)
+        st_cpair(sb, (const T*)nullptr, vb, N2 * k1 * srow, split_pair(b[k1], a[N1 - 1 - k1], scale));
     }
   }
 }
