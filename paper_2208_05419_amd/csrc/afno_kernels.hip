@@ -57,16 +57,21 @@ static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h, int kp
 }
 
 // Size-specialised W-axis kernels: (W, N1, N2, NP), W = N1 N2 split into an N2-point register
-// stage and an N1-point stage after the LDS exchange, NP complex signals per workgroup.  The
-// splits are the measured fastest per direction (W = 180: forward 12 x 15, inverse 15 x 12;
-// W = 360: 15 x 24 both ways); the slice width NP is the same in both lists.
-#define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 32) X(360, 15, 24, 16)
+// stage and an N1-point stage after the LDS exchange, NP complex signals (2 NP channels) per
+// workgroup.  Splits and slice widths are the measured fastest per direction (W = 180: forward
+// 12 x 15 on 32 channels, inverse 15 x 12 on 64; W = 360: 15 x 24 on 32 channels both ways).
+#define AFNO_ROW_FAST_LIST(X) X(32, 8, 4, 32) X(180, 12, 15, 16) X(360, 15, 24, 16)
 #define AFNO_ROW_INV_LIST(X) X(32, 8, 4, 32) X(180, 15, 12, 32) X(360, 15, 24, 16)
+// both directions specialised for W, and C a whole number of slices in each
 bool fast_row_available(int64_t W, int64_t C) {
-#define AFNO_CASE(w, n1, n2, np) if (W == w) return C % (2 * np) == 0;
+  bool fwd = false, inv = false;
+#define AFNO_CASE(w, n1, n2, np) if (W == w) fwd = C % (2 * np) == 0;
   AFNO_ROW_FAST_LIST(AFNO_CASE)
 #undef AFNO_CASE
-  return false;
+#define AFNO_CASE(w, n1, n2, np) if (W == w) inv = C % (2 * np) == 0;
+  AFNO_ROW_INV_LIST(AFNO_CASE)
+#undef AFNO_CASE
+  return fwd && inv;
 }
 
 bool fast_col_available(int dtype, int64_t H, int64_t bs) {
