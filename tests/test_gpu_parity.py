@@ -288,6 +288,14 @@ EDGE = [
     (1, 180, 24, 64, 2, "fp32", 0.01, 1.0),
     (2, 180, 12, 64, 2, "bf16", 0.01, 0.7),
     (1, 180, 20, 128, 2, "bf16", 0.01, 1.0),
+    # W-axis slices: the W = 180 forward on 32 channels and inverse on 64 (fp32: full 128-byte
+    # lines; channels not a multiple of 64 fall back to the generic W passes), W = 360 on 32
+    # channels (bf16 pairs of slices per line, a single slice per row, fp32)
+    (1, 20, 180, 128, 2, "fp32", 0.01, 1.0),
+    (1, 12, 180, 32, 1, "bf16", 0.01, 1.0),
+    (2, 9, 180, 96, 1, "bf16", 0.01, 0.8),
+    (1, 12, 360, 32, 1, "fp32", 0.01, 0.7),
+    (2, 10, 360, 32, 1, "bf16", 0.01, 1.0),
 ]
 
 
