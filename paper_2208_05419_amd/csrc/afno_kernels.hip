@@ -47,10 +47,14 @@ namespace afno {
 //   float one would not fit the LDS).
 int mfma_col_hp(int64_t H) { return H <= 32 ? 32 : (H <= 64 ? 64 : 96); }
 
-// tasks of the preparation job: the fragment-ordered weights' words, and the DFT table's
-// columns if with_tab
-static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h, int kp = 0) {
+size_t hidden_frag_bytes(const Plan& pl);
+
+// tasks of the preparation job: the fragment-ordered weights' words (hidden = true: the
+// hidden-size kernel's), and the DFT table's columns if with_tab
+static int64_t prep_words_host(const Plan& pl, bool with_tab, int kept_h, int kp = 0,
+                               bool hidden = false) {
   const int hp = mfma_col_hp(pl.H);
+  if (hidden) return (int64_t)hidden_frag_bytes(pl) / 16 + (with_tab ? 2 * hp : 0);
   return pl.nb * (pl.dtype == 0 ? frag_words_per_block<float>((int)pl.bs)
                                 : frag_words_per_block<bf16>((int)pl.bs)) +
          (with_tab ? (kp > 0 ? kept_table_tasks(hp, kp) : dft_table_tasks(hp, kept_h)) : 0);
@@ -88,7 +92,7 @@ static void launch_row_fwd_fast(const Plan& pl, const T* x, T* S, PrepJob<T> pj,
   if (pl.W == w) {                                                                        \
     const unsigned nmain = (unsigned)row_grid<np, (int)sizeof(T)>(gx, (int)(pl.C / (2 * np))); \
     const unsigned nprep = pj.wout ? (unsigned)(std::min<int64_t>(                        \
-        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp) + np * n1 - 1) / (np * n1), 1024) \
+        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp, pj.hs > 0) + np * n1 - 1) / (np * n1), 1024) \
         + 7) / 8 * 8 : 0;                                                                 \
     pj.nprep = (int)nprep;                                                                \
     hipLaunchKernelGGL((row_r2c_fast<T, w, n1, n2, np>), dim3(nprep + nmain),              \
@@ -288,27 +292,19 @@ static hipError_t launch_all(const Plan& pl, const void* x, const void* w1, cons
   PrepJob<T> pj{static_cast<const T*>(w1), static_cast<const T*>(w2), nullptr, nullptr,
                 (int)pl.nb, (int)pl.bs, (int)pl.H, mfma_col_hp(pl.H), 0, (int)pl.kept_h,
                 stage == kStageSpectrum ? 0 : mfma_kept_rows(pl)};
-  if (col_mfma || col_fast)
+  if (col_mfma || col_fast || (sizeof(T) == 2 && col_hid))
     pj.wout = reinterpret_cast<typename FragWord<T>::type*>(static_cast<char*>(S) + pl.frag_offset);
-  if (col_mfma) pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
+  if (col_mfma || (sizeof(T) == 2 && col_hid))
+    pj.tout = reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset);
+  if (sizeof(T) == 2 && col_hid) pj.hs = (int)pl.col.hs;  // the hidden-size kernel's fragments
   // ev[0]: recorded only before a preparation launch of its own (a preparation inside the W-axis
   // forward launch belongs to that phase; the profile counts an unrecorded ev[0] as zero)
-  const bool prep_launch = (pj.wout && !row_fast) || (sizeof(T) == 2 && col_hid);
+  const bool prep_launch = pj.wout && !row_fast;
   if (ev && prep_launch) (void)hipEventRecord(ev[0], st);
-  if (pj.wout && !row_fast) {
-    const unsigned g = (unsigned)std::min<int64_t>((prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp) + 255) / 256, 4096);
+  if (prep_launch) {
+    const unsigned g = (unsigned)std::min<int64_t>(
+        (prep_words_host(pl, pj.tout != nullptr, pj.kept_h, pj.kp, pj.hs > 0) + 255) / 256, 4096);
     hipLaunchKernelGGL(prep_operands_kernel<T>, dim3(g), dim3(256), 0, st, pj);
-  }
-  if constexpr (sizeof(T) == 2) {
-    if (col_hid) {  // the hidden-size kernel's fragments and the DFT table, a launch of their own
-      const int hp = mfma_col_hp(pl.H);
-      const int64_t words = (int64_t)hidden_frag_bytes(pl) / 16 + 2 * hp;
-      hipLaunchKernelGGL(prep_hidden_kernel, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 4096)),
-                         dim3(256), 0, st, static_cast<const bf16*>(w1), static_cast<const bf16*>(w2),
-                         reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.frag_offset),
-                         reinterpret_cast<uint4*>(static_cast<char*>(S) + pl.tab_offset),
-                         (int)pl.nb, (int)pl.bs, (int)pl.col.hs, (int)pl.H, hp, (int)pl.kept_h);
-    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

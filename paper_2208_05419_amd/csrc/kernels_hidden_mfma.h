@@ -30,55 +30,9 @@ struct MfmaHid {
   static_assert(MH % G::MT == 0, "hidden tiles a multiple of the block's");
 };
 
-// fragment words of the hidden-size block weights (and, appended, the DFT table's 2 HP column
-// tasks, dft_table_column), i, i + stride, ...: per block, layer 1 then layer 2 as above
-__device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, const bf16* w1,
-                                                  const bf16* w2, uint4* wout, uint4* tout,
-                                                  int nb, int bs, int hs, int H, int HP,
-                                                  int kept_h, const float2* roots) {
-  const int mh = 2 * hs / 16, mt = 2 * bs / 16;
-  const int64_t l1 = (int64_t)(2 * bs / 32) * mh * 64;
-  const int64_t per_block = 2 * l1;
-  const int64_t nw = (int64_t)nb * per_block;
-  // the table's column tasks first: each is a sequential pass over a column, so they start
-  // in the launch's first workgroup
-  const int64_t ntab = tout ? (int64_t)2 * HP : 0;
-  const int64_t total = nw + ntab;
-  for (; i < total; i += stride) {
-    if (i < ntab) {
-      dft_table_column((int)i, H, HP, kept_h, roots, tout);
-      continue;
-    }
-    const int64_t q = i - ntab;  // weight word q
-    const int64_t blk = q / per_block;
-    int64_t u = q - blk * per_block;
-    const int layer = u >= l1 ? 1 : 0;
-    u -= layer * l1;
-    const int lane = (int)(u & 63);
-    const int64_t f = u >> 6;
-    const int nt = layer ? mt : mh;                 // output tiles of the layer
-    const int t = (int)(f % nt), s = (int)(f / nt);
-    const bf16* w = layer ? w2 + blk * (int64_t)hs * bs * 2 : w1 + blk * (int64_t)bs * hs * 2;
-    const int n_out = layer ? bs : hs;
-    const int j = (16 * t + (lane & 15)) >> 1;
-    wout[q] = FragWord<bf16>::make(w, n_out, s * 32, j, lane & 1, lane);
-  }
-}
-
-__global__ void __launch_bounds__(256) prep_hidden_kernel(const bf16* __restrict__ w1,
-                                                          const bf16* __restrict__ w2,
-                                                          uint4* __restrict__ wout,
-                                                          uint4* __restrict__ tout, int nb, int bs,
-                                                          int hs, int H, int HP, int kept_h) {
-  __shared__ float2 roots[96];
-  dft_roots(roots, H);
-  prep_hidden_words(blockIdx.x * (int64_t)blockDim.x + threadIdx.x,
-                    (int64_t)gridDim.x * blockDim.x, w1, w2, wout, tout, nb, bs, hs, H, HP, kept_h,
-                    roots);
-}
-
 // grid B * KW * nb (block index fastest), 512 threads, dynamic LDS MfmaHid<HP, BS, HS>::kBytes.
-// S: spectrum [B][H][KW][C] complex bf16, updated in place; wfrag, dtab from prep_hidden_kernel.
+// S: spectrum [B][H][KW][C] complex bf16, updated in place; wfrag, dtab from prep_operands
+// (a job with hs set).
 template <int HP, int BS, int HS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 column_mfma_hidden(bf16* __restrict__ S, const uint4* __restrict__ wfrag,

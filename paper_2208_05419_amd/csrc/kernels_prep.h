@@ -153,6 +153,42 @@ __device__ __forceinline__ void kept_table_task(int64_t i, int H, int HP, int KP
   }
 }
 
+// fragment words of the hidden-size block weights (bf16, hidden size hs: per block layer 1,
+// (2 bs / 32) k-steps x (2 hs / 16) n-tiles, then layer 2, (2 hs / 32) x (2 bs / 16)), after
+// the DFT table's 2 HP column tasks (dft_table_column), tasks i, i + stride, ...
+__device__ __forceinline__ void prep_hidden_words(int64_t i, int64_t stride, const bf16* w1,
+                                                  const bf16* w2, uint4* wout, uint4* tout,
+                                                  int nb, int bs, int hs, int H, int HP,
+                                                  int kept_h, const float2* roots) {
+  const int mh = 2 * hs / 16, mt = 2 * bs / 16;
+  const int64_t l1 = (int64_t)(2 * bs / 32) * mh * 64;
+  const int64_t per_block = 2 * l1;
+  const int64_t nw = (int64_t)nb * per_block;
+  // the table's column tasks first: each is a sequential pass over a column, so they start
+  // in the launch's first workgroup
+  const int64_t ntab = tout ? (int64_t)2 * HP : 0;
+  const int64_t total = nw + ntab;
+  for (; i < total; i += stride) {
+    if (i < ntab) {
+      dft_table_column((int)i, H, HP, kept_h, roots, tout);
+      continue;
+    }
+    const int64_t q = i - ntab;  // weight word q
+    const int64_t blk = q / per_block;
+    int64_t u = q - blk * per_block;
+    const int layer = u >= l1 ? 1 : 0;
+    u -= layer * l1;
+    const int lane = (int)(u & 63);
+    const int64_t f = u >> 6;
+    const int nt = layer ? mt : mh;                 // output tiles of the layer
+    const int t = (int)(f % nt), s = (int)(f / nt);
+    const bf16* w = layer ? w2 + blk * (int64_t)hs * bs * 2 : w1 + blk * (int64_t)bs * hs * 2;
+    const int n_out = layer ? bs : hs;
+    const int j = (16 * t + (lane & 15)) >> 1;
+    wout[q] = FragWord<bf16>::make(w, n_out, s * 32, j, lane & 1, lane);
+  }
+}
+
 // What to prepare: both layers of every block in fragment order (frag_words_per_block words
 // per block, word ((layer * KSTEPS + s) * NT16 + t) * 64 + lane), then, if tout is set, the
 // DFT table for height H padded to HP: kept_h >= 0, 2 HP column tasks (dft_table_column, the
@@ -168,6 +204,7 @@ struct PrepJob {
   int nprep;   // workgroups the host launch gives the job (placed before its own work)
   int kept_h;  // the table's rounding, as above
   int kp;      // > 0: the kept-row kernel's two tables for kp kept rows (kept_table_task)
+  int hs;      // > 0 and != bs (bf16): the hidden-size kernel's fragments (prep_hidden_words)
 };
 
 __host__ __device__ inline int64_t dft_table_tasks(int HP, int kept_h) {
@@ -176,6 +213,8 @@ __host__ __device__ inline int64_t dft_table_tasks(int HP, int kept_h) {
 
 template <typename T>
 __device__ __forceinline__ int64_t prep_words(const PrepJob<T>& pj) {
+  if (sizeof(T) == 2 && pj.hs > 0 && pj.hs != pj.bs)
+    return (int64_t)pj.nb * 2 * (2 * pj.bs / 32) * (2 * pj.hs / 16) * 64 + (pj.tout ? 2 * pj.HP : 0);
   return (int64_t)pj.nb * frag_words_per_block<T>(pj.bs) +
          (pj.tout ? (pj.kp > 0 ? kept_table_tasks(pj.HP, pj.kp) : dft_table_tasks(pj.HP, pj.kept_h))
                   : 0);
@@ -186,6 +225,13 @@ __device__ __forceinline__ int64_t prep_words(const PrepJob<T>& pj) {
 template <typename T>
 __device__ void prep_operands(int64_t i, int64_t stride, const PrepJob<T>& pj,
                               const float2* roots) {
+  if constexpr (sizeof(T) == 2) {
+    if (pj.hs > 0 && pj.hs != pj.bs) {
+      prep_hidden_words(i, stride, pj.w1, pj.w2, pj.wout, pj.tout, pj.nb, pj.bs, pj.hs, pj.H,
+                        pj.HP, pj.kept_h, roots);
+      return;
+    }
+  }
   const int nt16 = 2 * pj.bs / 16, ksteps = 2 * pj.bs / Mma<T>::kK;
   const int64_t nw = (int64_t)pj.nb * frag_words_per_block<T>(pj.bs);
   const int64_t total = prep_words(pj);
